@@ -1,0 +1,3 @@
+"""CPU float64 oracle (test infrastructure only; see oracle.naive)."""
+from .naive import *  # noqa: F401,F403
+from .naive import __all__  # noqa: F401
