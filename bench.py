@@ -1,0 +1,205 @@
+"""Benchmark of the fused attention forward+backward pass on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+One step is one attn_fwd_bwd call (forward, dK/dV and dQ kernels) over the
+whole workload, inputs resident in HBM before timing starts. Prints ONE JSON
+line with whole-job TFLOP/s (algorithmic flops 14*d per (query, key) pair
+that takes part), the roofline position of the dominant kernel measured with
+HIP events on the launch stream, the max relative error of every output on a
+sampled head against the float64 oracle, and the oracle itself timed on the
+host as a CPU baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads  # noqa: E402
+
+METRIC = "fused attn fwd+bwd TFLOP/s and % of MI355X MFMA peak (1 GPU); max rel err"
+DEFAULT_WORKLOAD = "b2h32_n16384_d128_bf16_causal"
+# MI355X published dense peaks (TFLOP/s)
+PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
+HBM_PEAK_GBS = 8000.0
+KERNELS = ("fwd", "dkdv", "dq")
+# algorithmic flops per (query, key) pair and per d, by kernel: the forward's
+# two products; the dK/dV kernel's S recompute, dP, dV and dK; the dQ kernel's
+# dQ product (its S and dP recomputation is counted once, in dK/dV).
+ALG_FLOPS_PER_PAIR_D = {"fwd": 4, "dkdv": 8, "dq": 2}
+# flops the MFMA units execute per pair and per d, by kernel
+EXEC_FLOPS_PER_PAIR_D = {"fwd": 4, "dkdv": 8, "dq": 6}
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime that torch already loaded."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        ev = ctypes.c_void_p()
+        rc = self.hip.hipEventCreate(ctypes.byref(ev))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed ({rc})")
+        return ev.value
+
+    def elapsed_ms(self, a, b) -> float:
+        out = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(out), a, b)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(out.value)
+
+    def destroy(self, ev):
+        self.hip.hipEventDestroy(ev)
+
+
+def cpu_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        n = [p.get("num_threads", 0) for p in threadpool_info() if p.get("user_api") == "blas"]
+        if n:
+            return int(max(n))
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0))
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the host oracle (and with it the sampled-head error check)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): every (batch, head) is "
+              "independent, so a multi-GPU run would shard heads with no communication; "
+              "run with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2609_33916_amd as attn
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    w = workloads.WORKLOADS[args.workload]
+    print(f"[bench] workload {w.name}: generating seeded inputs", file=sys.stderr, flush=True)
+    inp = workloads.generate(w)
+    dev = workloads.to_torch(inp, "cuda")
+    q, k, v, do = dev["q"], dev["k"], dev["v"], dev["do"]
+    B, H, n, d = q.shape
+    O = torch.empty_like(q)
+    L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
+    dQ, dK, dV = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    ws = torch.empty(attn.attn_workspace_bytes(B, H, n, d), dtype=torch.uint8, device=q.device)
+    out = (O, L, dQ, dK, dV)
+
+    hip = HipEvents()
+    evs = [[hip.create() for _ in range(4)] for _ in range(args.steps)]
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        attn.attn_fwd_bwd(q, k, v, do, scale=w.scale, causal=w.causal, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        attn.attn_fwd_bwd_timed(q, k, v, do, evs[i], scale=w.scale, causal=w.causal, out=out,
+                                workspace=ws)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    wall_ms = (t1 - t0) * 1e3 / args.steps
+    per_kernel = {name: [hip.elapsed_ms(e[j], e[j + 1]) for e in evs] for j, name in enumerate(KERNELS)}
+    step_dev = [hip.elapsed_ms(e[0], e[3]) for e in evs]
+    for e in evs:
+        for x in e:
+            hip.destroy(x)
+
+    pairs = workloads.causal_pairs(n, w.causal) * B * H
+    f_alg = workloads.alg_flops(B, H, n, d, w.causal)
+    value = f_alg / (wall_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.dtype]
+    kstats = {}
+    for name in KERNELS:
+        mean_ms = statistics.fmean(per_kernel[name])
+        kstats[name] = {
+            "mean_ms": round(mean_ms, 4),
+            "alg_tflops": round(ALG_FLOPS_PER_PAIR_D[name] * d * pairs / (mean_ms * 1e-3) / 1e12, 2),
+            "mfma_exec_tflops": round(EXEC_FLOPS_PER_PAIR_D[name] * d * pairs / (mean_ms * 1e-3) / 1e12, 2),
+        }
+    dom = max(KERNELS, key=lambda nme: kstats[nme]["mean_ms"])
+    dom_alg_flops = ALG_FLOPS_PER_PAIR_D[dom] * d * pairs
+    achieved = dom_alg_flops / (kstats[dom]["mean_ms"] * 1e-3) / 1e12
+
+    record = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 4),
+        "device_ms_per_step": round(statistics.median(step_dev), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "pct_of_peak": round(100.0 * value / peak, 2),
+        "config": {"workload": w.name, "B": B, "H": H, "n": n, "d": d, "causal": w.causal,
+                   "dtype": w.dtype, "scale": w.scale, "alg_flops": f_alg,
+                   "parallelism": "single GPU, one workgroup per (head, tile)"},
+        "kernels": kstats,
+        "roofline": {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None},
+    }
+
+    if not args.no_cpu_baseline:
+        import oracle
+        from oracle import naive
+        b, h = B - 1, H // 2 + 3 if H > 3 else H - 1
+        threads = cpu_threads()
+        print(f"[bench] cpu baseline: oracle on head (b={b}, h={h}) with {threads} threads",
+              file=sys.stderr, flush=True)
+        c0 = time.perf_counter()
+        ref = naive.attention_head(inp.q[b, h], inp.k[b, h], inp.v[b, h], inp.do[b, h], w.scale,
+                                   w.causal)
+        c1 = time.perf_counter()
+        head_flops = workloads.alg_flops(1, 1, n, d, w.causal)
+        got = {"O": O[b, h], "L": L[b, h], "dQ": dQ[b, h], "dK": dK[b, h], "dV": dV[b, h]}
+        errs = {key: oracle.max_rel_err(t.float().cpu().numpy(), ref[key]) for key, t in got.items()}
+        record["max_rel_err"] = {key: float(f"{val:.3e}") for key, val in errs.items()}
+        record["max_rel_err_sample"] = f"head (b={b}, h={h}) of {B * H}, all outputs, vs float64 oracle"
+        record["cpu_baseline"] = {
+            "value": round(head_flops / (c1 - c0) / 1e12, 6),
+            "unit": "TFLOP/s",
+            "cores": threads,
+            "kind": "oracle",
+            "sample": f"1 of {B * H} heads (n={n}, d={d}), float64 NumPy naive fwd+bwd with "
+                      f"explicit n x n S and P, {c1 - c0:.1f} s",
+        }
+    print(json.dumps(record), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

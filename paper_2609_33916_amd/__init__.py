@@ -1,0 +1,168 @@
+"""Fused attention forward+backward for AMD Instinct MI355X (gfx950).
+
+A thin ctypes binding over the C ABI of ``libattn_mi355x.so`` (declared in
+``include/attn_mi355x.h``). The binding only marshals arguments: every step of
+the computation runs in the library's HIP kernels. PyTorch provides device
+memory and the current stream.
+
+    O, L = attn_fwd(q, k, v, scale, causal)
+    O, L, dQ, dK, dV = attn_fwd_bwd(q, k, v, do, scale, causal)
+
+Tensors are contiguous [B, H, n, d] on one GPU, all bfloat16 or all float32;
+L is float32 [B, H, n] (natural-log log-sum-exp of the scaled, masked scores).
+There is no fallback: if the library is missing or the device is not a GPU,
+the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Tuple
+
+import torch  # loads the process's HIP runtime before the library
+
+__all__ = ["attn_fwd", "attn_fwd_bwd", "attn_fwd_bwd_timed", "attn_workspace_bytes", "attn_strerror",
+           "AttnError", "lib", "LIB_PATH", "ATTN_BF16", "ATTN_F32"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libattn_mi355x.so")
+ATTN_BF16 = 0
+ATTN_F32 = 1
+
+_lib = None
+
+
+class AttnError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        super().__init__(f"{where} failed with code {code}: {attn_strerror(code)}")
+        self.code = code
+
+
+def lib() -> ctypes.CDLL:
+    """Load libattn_mi355x.so (once) and declare the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2609_33916_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i, f, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    L.attn_workspace_bytes.argtypes = [i, i, i, i]
+    L.attn_workspace_bytes.restype = sz
+    L.attn_fwd.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
+    L.attn_fwd.restype = i
+    L.attn_fwd_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                               i, i, i, i, f, i, i, vp]
+    L.attn_fwd_bwd.restype = i
+    L.attn_fwd_bwd_timed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                     i, i, i, i, f, i, i, vp, ctypes.POINTER(vp)]
+    L.attn_fwd_bwd_timed.restype = i
+    L.attn_strerror.argtypes = [i]
+    L.attn_strerror.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def attn_strerror(code: int) -> str:
+    return lib().attn_strerror(int(code)).decode()
+
+
+def attn_workspace_bytes(B: int, H: int, n: int, d: int) -> int:
+    return int(lib().attn_workspace_bytes(B, H, n, d))
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return ATTN_BF16
+    if t.dtype == torch.float32:
+        return ATTN_F32
+    raise TypeError(f"unsupported dtype {t.dtype} (bfloat16 or float32)")
+
+
+def _check(name: str, t: torch.Tensor, ref: torch.Tensor) -> None:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != ref.dtype or t.shape != ref.shape or t.device != ref.device:
+        raise ValueError(f"{name} must match q in dtype, shape and device")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _stream(dev: torch.device) -> int:
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def _scale(scale: Optional[float], d: int) -> float:
+    return 1.0 / math.sqrt(d) if scale is None else float(scale)
+
+
+def attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: Optional[float] = None,
+             causal: bool = False, out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None):
+    """Forward pass: returns (O, L). ``scale`` defaults to 1/sqrt(d)."""
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, n, d]")
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(name, t, q)
+    B, H, n, d = q.shape
+    if out is None:
+        O = torch.empty_like(q)
+        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
+    else:
+        O, L = out
+    rc = lib().attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), O.data_ptr(), L.data_ptr(),
+                        B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
+                        _stream(q.device))
+    if rc != 0:
+        raise AttnError(rc, "attn_fwd")
+    return O, L
+
+
+def attn_fwd_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, do: torch.Tensor,
+                 scale: Optional[float] = None, causal: bool = False,
+                 out: Optional[Tuple[torch.Tensor, ...]] = None,
+                 workspace: Optional[torch.Tensor] = None):
+    """Fused forward+backward: returns (O, L, dQ, dK, dV).
+
+    ``out`` may supply preallocated (O, L, dQ, dK, dV) and ``workspace`` a
+    uint8 GPU tensor of at least attn_workspace_bytes(B, H, n, d) bytes."""
+    return _fwd_bwd(q, k, v, do, scale, causal, out, workspace, None)
+
+
+def attn_fwd_bwd_timed(q, k, v, do, events, scale: Optional[float] = None, causal: bool = False,
+                       out=None, workspace=None):
+    """attn_fwd_bwd that records 4 caller-created hipEvent_t handles (ints)
+    around its three kernels on the current stream."""
+    if len(events) != 4:
+        raise ValueError("events must hold 4 hipEvent_t handles")
+    return _fwd_bwd(q, k, v, do, scale, causal, out, workspace, events)
+
+
+def _fwd_bwd(q, k, v, do, scale, causal, out, workspace, events):
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, n, d]")
+    for name, t in (("q", q), ("k", k), ("v", v), ("do", do)):
+        _check(name, t, q)
+    B, H, n, d = q.shape
+    if out is None:
+        O = torch.empty_like(q)
+        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
+        dQ, dK, dV = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    else:
+        O, L, dQ, dK, dV = out
+    wsb = attn_workspace_bytes(B, H, n, d)
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
+            O.data_ptr(), L.data_ptr(), dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
+            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+            B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q), _stream(q.device))
+    if events is None:
+        rc = lib().attn_fwd_bwd(*args)
+        where = "attn_fwd_bwd"
+    else:
+        arr = (ctypes.c_void_p * 4)(*events)
+        rc = lib().attn_fwd_bwd_timed(*args, arr)
+        where = "attn_fwd_bwd_timed"
+    if rc != 0:
+        raise AttnError(rc, where)
+    return O, L, dQ, dK, dV

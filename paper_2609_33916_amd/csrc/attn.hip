@@ -1,0 +1,212 @@
+// C ABI of the attention library (declared in include/attn_mi355x.h):
+// argument validation, kernel selection by (dtype, d, causal) and launches.
+// Validation happens entirely on the host before any HIP call, so every
+// error code can be exercised without a GPU.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <limits>
+
+#include "attn_mi355x.h"
+#include "kernels.hpp"
+
+namespace {
+
+using attn::bf16;
+
+constexpr int kFwdBQ = 128;   // queries per forward / dQ workgroup
+constexpr int kDkvBKV = 128;  // keys per dK/dV workgroup
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+int check_common(int B, int H, int n, int d, float scale, int causal, int dtype) {
+  if (B < 1 || H < 1 || n < 1) return ATTN_E_SHAPE;
+  if (dtype != ATTN_BF16 && dtype != ATTN_F32) return ATTN_E_UNSUPPORTED;
+  if (d != 32 && d != 64 && d != 128) return ATTN_E_UNSUPPORTED;
+  if (!std::isfinite(scale)) return ATTN_E_ARG;
+  if (causal != 0 && causal != 1) return ATTN_E_ARG;
+  // grid sizes and per-head element offsets must fit in int
+  const long long heads = (long long)B * H;
+  const long long tiles = (n + 63) / 64;
+  if ((long long)n * d > std::numeric_limits<int>::max()) return ATTN_E_SHAPE;
+  if (heads * tiles > std::numeric_limits<int>::max()) return ATTN_E_SHAPE;
+  return ATTN_OK;
+}
+
+struct ScaleParts {
+  float sl2;
+  float abs_scale;
+  uint32_t qflip;  // per-dword sign mask for Q elements
+};
+
+ScaleParts split_scale(float scale, int dtype) {
+  ScaleParts s;
+  s.abs_scale = std::fabs(scale);
+  // a zero scale would turn masked scores (-inf) into NaN; a floor far below
+  // any representable score difference keeps them at -inf and leaves P exact
+  s.sl2 = std::fmax(s.abs_scale * attn::kLog2e, 1e-30f);
+  const bool neg = std::signbit(scale) && scale != 0.f;
+  s.qflip = neg ? (dtype == ATTN_BF16 ? 0x80008000u : 0x80000000u) : 0u;
+  return s;
+}
+
+template <typename T, int D, bool CAUSAL>
+void launch_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
+  a.ntiles = (a.n + kFwdBQ - 1) / kFwdBQ;
+  a.nblocks = heads * a.ntiles;
+  hipLaunchKernelGGL((attn::fwd_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
+}
+
+template <typename T, int D, bool CAUSAL>
+void launch_dkdv(attn::BwdArgs a, int heads, hipStream_t st) {
+  a.ntiles = (a.n + kDkvBKV - 1) / kDkvBKV;
+  a.nblocks = heads * a.ntiles;
+  hipLaunchKernelGGL((attn::dkdv_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
+}
+
+template <typename T, int D, bool CAUSAL>
+void launch_dq(attn::BwdArgs a, int heads, hipStream_t st) {
+  a.ntiles = (a.n + kFwdBQ - 1) / kFwdBQ;
+  a.nblocks = heads * a.ntiles;
+  hipLaunchKernelGGL((attn::dq_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
+}
+
+template <typename T, int D, bool C>
+struct FwdL { static void run(attn::FwdArgs a, int heads, hipStream_t st) { launch_fwd<T, D, C>(a, heads, st); } };
+template <typename T, int D, bool C>
+struct DkvL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { launch_dkdv<T, D, C>(a, heads, st); } };
+template <typename T, int D, bool C>
+struct DqL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { launch_dq<T, D, C>(a, heads, st); } };
+
+template <template <typename, int, bool> class F, typename T, typename Args>
+void by_d(int d, int causal, Args a, int heads, hipStream_t st) {
+  if (d == 32) { causal ? F<T, 32, true>::run(a, heads, st) : F<T, 32, false>::run(a, heads, st); }
+  else if (d == 64) { causal ? F<T, 64, true>::run(a, heads, st) : F<T, 64, false>::run(a, heads, st); }
+  else { causal ? F<T, 128, true>::run(a, heads, st) : F<T, 128, false>::run(a, heads, st); }
+}
+
+template <template <typename, int, bool> class F, typename Args>
+void run_dispatch(int dtype, int d, int causal, Args a, int heads, hipStream_t st) {
+  if (dtype == ATTN_BF16) by_d<F, bf16>(d, causal, a, heads, st);
+  else by_d<F, float>(d, causal, a, heads, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t attn_workspace_bytes(int B, int H, int n, int d) {
+  (void)d;
+  if (B < 1 || H < 1 || n < 1) return 0;
+  return (size_t)B * (size_t)H * (size_t)n * sizeof(float);
+}
+
+int attn_fwd(const void* Q, const void* K, const void* V, void* O, float* L,
+             int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
+  if (!Q || !K || !V || !O || !L) return ATTN_E_NULL;
+  int rc = check_common(B, H, n, d, scale, causal, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(L, 4))
+    return ATTN_E_ALIGN;
+  const ScaleParts sp = split_scale(scale, dtype);
+  attn::FwdArgs a{};
+  a.q = Q; a.k = K; a.v = V; a.dout = nullptr;
+  a.o = O; a.lse = L; a.dvec = nullptr;
+  a.head_stride = (long long)n * d;
+  a.n = n;
+  a.sl2 = sp.sl2;
+  a.qflip = sp.qflip;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  run_dispatch<FwdL>(dtype, d, causal, a, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  return ATTN_OK;
+}
+
+static int fwd_bwd_impl(const void* Q, const void* K, const void* V, const void* dO,
+                        void* O, float* L, void* dQ, void* dK, void* dV,
+                        void* workspace, size_t workspace_bytes,
+                        int B, int H, int n, int d, float scale, int causal, int dtype,
+                        void* stream, void* const* events) {
+  if (!Q || !K || !V || !dO || !O || !L || !dQ || !dK || !dV || !workspace) return ATTN_E_NULL;
+  int rc = check_common(B, H, n, d, scale, causal, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(dO, 16) ||
+      !aligned(O, 16) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) ||
+      !aligned(L, 4) || !aligned(workspace, 4))
+    return ATTN_E_ALIGN;
+  if (workspace_bytes < attn_workspace_bytes(B, H, n, d)) return ATTN_E_WORKSPACE;
+  if (events) {
+    for (int i = 0; i < 4; ++i)
+      if (!events[i]) return ATTN_E_NULL;
+  }
+  const ScaleParts sp = split_scale(scale, dtype);
+  float* dvec = static_cast<float*>(workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  auto mark = [&](int i) {
+    return !events || hipEventRecord(static_cast<hipEvent_t>(events[i]), st) == hipSuccess;
+  };
+
+  attn::FwdArgs f{};
+  f.q = Q; f.k = K; f.v = V; f.dout = dO;
+  f.o = O; f.lse = L; f.dvec = dvec;
+  f.head_stride = (long long)n * d;
+  f.n = n;
+  f.sl2 = sp.sl2;
+  f.qflip = sp.qflip;
+
+  attn::BwdArgs b{};
+  b.q = Q; b.k = K; b.v = V; b.dout = dO;
+  b.lse = L; b.dvec = dvec;
+  b.dq = dQ; b.dk = dK; b.dv = dV;
+  b.head_stride = (long long)n * d;
+  b.n = n;
+  b.sl2 = sp.sl2;
+  b.dk_scale = sp.abs_scale;
+  b.dq_scale = scale;
+  b.qflip = sp.qflip;
+
+  if (!mark(0)) return ATTN_E_HIP;
+  run_dispatch<FwdL>(dtype, d, causal, f, B * H, st);
+  if (hipGetLastError() != hipSuccess || !mark(1)) return ATTN_E_HIP;
+  run_dispatch<DkvL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess || !mark(2)) return ATTN_E_HIP;
+  run_dispatch<DqL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess || !mark(3)) return ATTN_E_HIP;
+  return ATTN_OK;
+}
+
+int attn_fwd_bwd(const void* Q, const void* K, const void* V, const void* dO,
+                 void* O, float* L, void* dQ, void* dK, void* dV,
+                 void* workspace, size_t workspace_bytes,
+                 int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
+  return fwd_bwd_impl(Q, K, V, dO, O, L, dQ, dK, dV, workspace, workspace_bytes,
+                      B, H, n, d, scale, causal, dtype, stream, nullptr);
+}
+
+int attn_fwd_bwd_timed(const void* Q, const void* K, const void* V, const void* dO,
+                       void* O, float* L, void* dQ, void* dK, void* dV,
+                       void* workspace, size_t workspace_bytes,
+                       int B, int H, int n, int d, float scale, int causal, int dtype,
+                       void* stream, void* const* events) {
+  return fwd_bwd_impl(Q, K, V, dO, O, L, dQ, dK, dV, workspace, workspace_bytes,
+                      B, H, n, d, scale, causal, dtype, stream, events);
+}
+
+const char* attn_strerror(int code) {
+  switch (code) {
+    case ATTN_OK: return "success";
+    case ATTN_E_NULL: return "a required pointer is NULL";
+    case ATTN_E_SHAPE: return "B, H or n < 1, or the problem is too large to index";
+    case ATTN_E_UNSUPPORTED: return "unsupported head dimension (d must be 32, 64 or 128) or dtype";
+    case ATTN_E_ALIGN: return "a tensor is not 16-byte aligned (L and workspace: 4-byte)";
+    case ATTN_E_WORKSPACE: return "workspace smaller than attn_workspace_bytes()";
+    case ATTN_E_HIP: return "the HIP runtime rejected a kernel launch";
+    case ATTN_E_ARG: return "scale is not finite, or causal is not 0 or 1";
+    default: return "unknown attn status code";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,275 @@
+// Device building blocks for the gfx950 attention kernels: element traits,
+// matrix-core (MFMA) wrappers, LDS tile layout and operand reads, lane-half
+// reductions and the workgroup -> (head, tile) schedule.
+//
+// MFMA 32x32 register layouts (wave64, lane l, half h = l / 32, c = l % 32):
+//   A operand   : row c, k slots [h*KP, h*KP + KP)
+//   B operand   : col c, same k slots
+//   accumulator : col c, row R(h, j) = 8*(j/4) + 4*h + (j%4), j in [0, 16)
+// with KP = 8 for v_mfma_f32_32x32x16_bf16 and KP = 1 for
+// v_mfma_f32_32x32x2_f32. Only the accumulator layout matters for
+// correctness: any order of k slots works as long as A and B agree.
+//
+// Tiles in LDS are row-major (contiguous along d) with a small pad, and the
+// rows of every 32-row block are stored permuted (srow below) so that
+//  * a "row read" (A operand = tile rows, contraction over d) has lane c read
+//    stored row c, and its accumulator row R(h, j) is logical row 16h + j;
+//    lane half h then owns 16 consecutive logical rows, which is exactly the
+//    k-slot order the next product needs when the accumulator is reused as
+//    an operand (P and dS are never written to memory);
+//  * a "transposed read" (A operand = tile columns, contraction over rows)
+//    gets 8 consecutive logical rows per lane: for bf16 with two
+//    ds_read_b64_tr_b16 (4 rows x 16 columns per 16-lane group), for float32
+//    with one 4-byte read per MFMA.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace attn {
+
+typedef __bf16 bf16;
+typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define ATTN_LDS __attribute__((address_space(3)))
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+// The running row maximum used for the exponentials is only moved when the
+// true maximum exceeds it by more than this many powers of two; exponentials
+// then stay below 2^8 and most key tiles skip rescaling the accumulators.
+constexpr float kRescaleThresh = 8.0f;
+
+// ---------------------------------------------------------------- traits --
+template <typename T> struct Elem;
+template <> struct Elem<bf16> {
+  using frag = bf16x8;               // one MFMA operand per lane
+  static constexpr int KP = 8;       // k slots per lane per MFMA
+  static constexpr int PAD = 8;      // LDS row pad (elements)
+  static constexpr int CH = 8;       // elements per 16-byte chunk
+};
+template <> struct Elem<float> {
+  using frag = float;
+  static constexpr int KP = 1;
+  static constexpr int PAD = 1;
+  static constexpr int CH = 4;
+};
+
+// ------------------------------------------------------------------ MFMA --
+__device__ __forceinline__ void mma(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma(f32x16& acc, float a, float b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) z[j] = 0.f;
+  return z;
+}
+
+// ------------------------------------------------------- permuted rows --
+// perm32(r): logical row held by accumulator row r once operand rows are
+// read through srow; perm32_inv is its inverse.
+__host__ __device__ constexpr int perm32(int r) { return ((r >> 2) & 1) * 16 + (r >> 3) * 4 + (r & 3); }
+__host__ __device__ constexpr int perm32_inv(int x) { return ((x >> 2) & 3) * 8 + (x >> 4) * 4 + (x & 3); }
+// stored row of logical row x (permutation inside each 32-row block)
+__host__ __device__ constexpr int srow(int x) { return (x & ~31) | perm32_inv(x & 31); }
+
+// ------------------------------------------------------ lane-half ops --
+// Lanes c and c + 32 hold the two halves of the same accumulator column.
+__device__ __forceinline__ float halves_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float halves_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ------------------------------------------------------- conversions --
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  bf16 a = (bf16)lo, b = (bf16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+// Operand fragment for k-step t from 16 accumulator values that are already
+// in the order of the next product's k slots (see file comment).
+template <typename T> struct FragFromAcc;
+template <> struct FragFromAcc<bf16> {
+  __device__ __forceinline__ static bf16x8 get(const f32x16& v, int t) {
+    bf16x8 f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) f[i] = (bf16)v[8 * t + i];
+    return f;
+  }
+};
+template <> struct FragFromAcc<float> {
+  __device__ __forceinline__ static float get(const f32x16& v, int t) { return v[t]; }
+};
+
+// ----------------------------------------------------- global -> regs --
+// B-operand fragments of one matrix row (row index = accumulator column c):
+// for k-step t the lane holds columns [t*2KP + h*KP, +KP). `flip` XORs the
+// sign bits (used to negate Q when the scale is negative). Rows >= n read 0.
+template <typename T, int D> struct RowFrags;
+template <int D> struct RowFrags<bf16, D> {
+  static constexpr int TD = D / 16;
+  bf16x8 f[TD];
+  __device__ __forceinline__ void load(const bf16* g, int row, int n, int h, uint32_t flip) {
+#pragma unroll
+    for (int t = 0; t < TD; ++t) {
+      u32x4 x = {0u, 0u, 0u, 0u};
+      if (row < n) x = *(const u32x4*)(g + (size_t)row * D + 16 * t + 8 * h);
+      x ^= (u32x4){flip, flip, flip, flip};
+      f[t] = __builtin_bit_cast(bf16x8, x);
+    }
+  }
+};
+template <int D> struct RowFrags<float, D> {
+  static constexpr int TD = D / 2;
+  float f[TD];
+  __device__ __forceinline__ void load(const float* g, int row, int n, int h, uint32_t flip) {
+#pragma unroll
+    for (int t = 0; t < TD; ++t) {
+      uint32_t x = 0u;
+      if (row < n) x = __float_as_uint(g[(size_t)row * D + 2 * t + h]);
+      f[t] = __uint_as_float(x ^ flip);
+    }
+  }
+};
+
+// ---------------------------------------------------------- LDS tiles --
+// A ROWS x D tile, row stride LD = D + PAD elements, rows permuted by srow.
+template <typename T, int ROWS, int D> struct Tile {
+  using E = Elem<T>;
+  static constexpr int LD = D + E::PAD;
+  static constexpr int ELEMS = ROWS * LD;
+  static constexpr int CPR = D / E::CH;            // 16-byte chunks per row
+  static constexpr int NCH = ROWS * CPR;
+  static constexpr int NPT = (NCH + 255) / 256;    // chunks per thread
+};
+
+// Register staging of one tile: global -> registers (issued early) and
+// registers -> LDS (after the current tile's reads are done).
+template <typename T, int ROWS, int D> struct Stage {
+  using TL = Tile<T, ROWS, D>;
+  u32x4 r[TL::NPT];
+  __device__ __forceinline__ void load(const T* g, int row0, int n, int tid, uint32_t flip) {
+#pragma unroll
+    for (int i = 0; i < TL::NPT; ++i) {
+      const int ci = tid + 256 * i;
+      u32x4 x = {0u, 0u, 0u, 0u};
+      if (TL::NCH % 256 == 0 || ci < TL::NCH) {
+        const int row = ci / TL::CPR, cc = ci % TL::CPR;
+        if (row0 + row < n) x = *(const u32x4*)(g + (size_t)(row0 + row) * D + cc * Elem<T>::CH);
+      }
+      r[i] = x ^ (u32x4){flip, flip, flip, flip};
+    }
+  }
+  __device__ __forceinline__ void store(T* s, int tid) const {
+#pragma unroll
+    for (int i = 0; i < TL::NPT; ++i) {
+      const int ci = tid + 256 * i;
+      if (TL::NCH % 256 == 0 || ci < TL::NCH) {
+        const int row = ci / TL::CPR, cc = ci % TL::CPR;
+        T* p = s + srow(row) * TL::LD + cc * Elem<T>::CH;
+        if constexpr (sizeof(T) == 2) {
+          *(u32x4*)p = r[i];
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) ((uint32_t*)p)[e] = r[i][e];
+        }
+      }
+    }
+  }
+};
+
+// Row read: A operand = logical rows of 32-row block `rb` (stored row
+// 32*rb + c), k-step t over d.
+template <typename T, int LD> struct RowRead;
+template <int LD> struct RowRead<bf16, LD> {
+  __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int t, int h, int c) {
+    return *(const bf16x8*)(s + (32 * rb + c) * LD + 16 * t + 8 * h);
+  }
+};
+template <int LD> struct RowRead<float, LD> {
+  __device__ __forceinline__ static float get(const float* s, int rb, int t, int h, int c) {
+    return s[(32 * rb + c) * LD + 2 * t + h];
+  }
+};
+
+// Transposed read: A operand = column 32*db + c of the tile, contraction over
+// logical rows of block rb; k-step t covers logical rows 16h + t*KP + [0, KP).
+template <typename T, int LD> struct TransRead;
+template <int LD> struct TransRead<bf16, LD> {
+  __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int db, int t, int h, int c) {
+    // 16-lane group: source lane q = c % 16 reads stored row base + q/4 and
+    // columns [32db + 16*(c/16) + 4*(q%4), +4); the transpose hands lane c
+    // column 32db + c of those 4 rows.
+    const int q = c & 15;
+    const int row = 32 * rb + 16 * t + 4 * h + (q >> 2);   // logical 16h+8t+k -> stored 16t+4h+k
+    const int col = 32 * db + 16 * (c >> 4) + 4 * (q & 3);
+    const bf16* p0 = s + row * LD + col;
+    const bf16* p1 = p0 + 8 * LD;                             // logical +4 -> stored +8
+    i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p0));
+    i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p1));
+    // whole-register bit casts (element-wise 16-bit inserts are avoided)
+    const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+    return __builtin_bit_cast(bf16x8, (u32x4){a[0], a[1], b[0], b[1]});
+  }
+};
+template <int LD> struct TransRead<float, LD> {
+  __device__ __forceinline__ static float get(const float* s, int rb, int db, int t, int h, int c) {
+    return s[(32 * rb + perm32_inv(16 * h + t)) * LD + 32 * db + c];
+  }
+};
+
+// ------------------------------------------------------ output stores --
+// Accumulator of a transposed product: lane (h, c) holds, for j-quad a,
+// 4 consecutive columns 32*db + 8a + 4h + [0, 4) of its row.
+template <typename T> struct Quad;
+template <> struct Quad<bf16> {
+  __device__ __forceinline__ static void store(bf16* p, float a, float b, float c, float d) {
+    *(u32x2*)p = (u32x2){pack_bf16x2(a, b), pack_bf16x2(c, d)};
+  }
+  __device__ __forceinline__ static f32x4 load(const bf16* p) {
+    const u32x2 x = *(const u32x2*)p;
+    return (f32x4){__uint_as_float(x[0] << 16), __uint_as_float(x[0] & 0xffff0000u),
+                   __uint_as_float(x[1] << 16), __uint_as_float(x[1] & 0xffff0000u)};
+  }
+};
+template <> struct Quad<float> {
+  __device__ __forceinline__ static void store(float* p, float a, float b, float c, float d) {
+    *(f32x4*)p = (f32x4){a, b, c, d};
+  }
+  __device__ __forceinline__ static f32x4 load(const float* p) { return *(const f32x4*)p; }
+};
+
+// --------------------------------------------------------- scheduling --
+// Workgroup id -> (head, tile). Consecutive workgroup ids are dispatched
+// round-robin over the 8 XCDs (each with its own L2); remapping gives every
+// XCD a contiguous range of (head, tile) so the tiles of one head, which
+// share K and V, run on the same L2. With `reverse`, tiles of a head are
+// issued from the last (most work under a causal mask) to the first.
+__device__ __forceinline__ void block_map(int bid, int nblocks, int ntiles, bool reverse,
+                                          int& head, int& tile) {
+  const int per = nblocks >> 3;
+  int lin = bid;
+  if (bid < per * 8) lin = (bid & 7) * per + (bid >> 3);
+  head = lin / ntiles;
+  const int t = lin - head * ntiles;
+  tile = reverse ? ntiles - 1 - t : t;
+}
+
+}  // namespace attn

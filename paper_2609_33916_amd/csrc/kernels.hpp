@@ -1,0 +1,457 @@
+// The three kernels of the fused attention forward+backward pass on gfx950.
+//
+//   fwd_kernel  (query-owner)  O, L and the backward's row vector D
+//   dkdv_kernel (key-owner)    dK, dV; each workgroup owns a block of keys
+//                              and sweeps the query tiles that see them
+//   dq_kernel   (query-owner)  dQ; each workgroup owns a block of queries
+//                              and sweeps the key tiles they see
+//
+// The scores S and probabilities P of a tile live only in registers: they
+// are produced by one MFMA product and consumed as the operand of the next
+// (the fused path of Fig. fig:concept, section sec:dnf-onf-machines). Each
+// output element is written by exactly one lane and there are no atomics:
+// dV and dK are accumulated by the workgroup that owns the key block (the
+// per-key-column pass of Paper II, section sec:paper2-gv-fix) and dQ by the
+// workgroup that owns the query block, with S and dP recomputed instead of
+// persisting the score gradient (the persisted-gradient alternative costs an
+// n^2 re-read, Paper II, section sec:paper2-gk-mechanism).
+//
+// Scores are handled in the base-2 domain: x = S_raw * sl2 with
+// sl2 = |scale| * log2(e), P = 2^(x - m), and L is converted back to the
+// natural log on output. A negative scale is folded into Q's sign.
+#pragma once
+
+#include "common.hpp"
+
+namespace attn {
+
+struct FwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* dout;   // optional: when set, D_i = sum_c dO_ic O_ic is written
+  void* o;
+  float* lse;
+  float* dvec;
+  long long head_stride;  // n * d elements
+  int n;
+  int ntiles;    // query tiles per head
+  int nblocks;   // grid size
+  float sl2;     // |scale| * log2(e), clamped away from 0
+  uint32_t qflip;  // sign-bit mask applied to Q (negative scale)
+};
+
+struct BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* dout;
+  const float* lse;
+  const float* dvec;
+  void* dq;
+  void* dk;
+  void* dv;
+  long long head_stride;
+  int n;
+  int ntiles;
+  int nblocks;
+  float sl2;
+  float dk_scale;  // |scale|: Q is read sign-flipped when scale < 0
+  float dq_scale;  // scale
+  uint32_t qflip;
+};
+
+// ======================================================================
+// Forward: a workgroup owns BQ = 128 queries (32 per wave); K and V tiles of
+// BKV = 64 keys are staged in LDS (double-buffered through registers).
+// Per wave and key tile:  S^T = K Q^T (rows = keys, cols = the wave's 32
+// queries), online softmax per column, O^T += V^T P^T.
+// ======================================================================
+template <typename T, int D, bool CAUSAL>
+__global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
+  using E = Elem<T>;
+  using Frag = typename E::frag;
+  constexpr int BQ = 128, BKV = 64, NKB = BKV / 32, NDB = D / 32;
+  constexpr int KP = E::KP;
+  constexpr int TD = D / (2 * KP);   // k-steps over d
+  constexpr int T32 = 16 / KP;       // k-steps over a 32-row block
+  using TL = Tile<T, BKV, D>;
+  constexpr int LD = TL::LD;
+  __shared__ __attribute__((aligned(16))) T smem[2][2][TL::ELEMS];
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  int head, qt;
+  block_map(blockIdx.x, a.nblocks, a.ntiles, CAUSAL, head, qt);
+  const int n = a.n;
+  const size_t hoff = (size_t)head * (size_t)a.head_stride;
+  const T* Qg = (const T*)a.q + hoff;
+  const T* Kg = (const T*)a.k + hoff;
+  const T* Vg = (const T*)a.v + hoff;
+  const int q0 = qt * BQ, qw0 = q0 + 32 * w, qi = qw0 + c;
+
+  RowFrags<T, D> qf;
+  qf.load(Qg, qi, n, h, a.qflip);
+
+  const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
+  const int nt = (kv_end + BKV - 1) / BKV;
+
+  Stage<T, BKV, D> ks, vs;
+  ks.load(Kg, 0, n, tid, 0u);
+  vs.load(Vg, 0, n, tid, 0u);
+  ks.store(smem[0][0], tid);
+  vs.store(smem[0][1], tid);
+  __syncthreads();
+
+  f32x16 oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = zero16();
+  float m_use = -INFINITY, lsum = 0.f;
+  const float sl2 = a.sl2;
+
+  for (int it = 0; it < nt; ++it) {
+    const int kv0 = it * BKV;
+    const int st = it & 1;
+    if (it + 1 < nt) {
+      ks.load(Kg, kv0 + BKV, n, tid, 0u);
+      vs.load(Vg, kv0 + BKV, n, tid, 0u);
+    }
+    const bool active = !CAUSAL || kv0 <= qw0 + 31;
+    if (active) {
+      const T* kl = smem[st][0];
+      const T* vl = smem[st][1];
+      f32x16 s[NKB];
+#pragma unroll
+      for (int b = 0; b < NKB; ++b) {
+        s[b] = zero16();
+#pragma unroll
+        for (int t = 0; t < TD; ++t) mma(s[b], RowRead<T, LD>::get(kl, b, t, h, c), qf.f[t]);
+      }
+      // lane (h, c): s[b][j] = raw score of key kv0 + 32b + 16h + j, query qi
+      const bool edge = (kv0 + BKV > n) || (CAUSAL && kv0 + BKV - 1 > qw0);
+      if (edge) {
+#pragma unroll
+        for (int b = 0; b < NKB; ++b)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int key = kv0 + 32 * b + 16 * h + j;
+            if (key >= n || (CAUSAL && key > qi)) s[b][j] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int b = 0; b < NKB; ++b)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[b][j]);
+      mx = halves_max(mx);
+      const float mt = mx * sl2;
+      const bool resc = mt > m_use + kRescaleThresh;
+      if (__builtin_amdgcn_ballot_w64(resc)) {
+        const float alpha = resc ? exp2_fast(m_use - mt) : 1.f;
+        if (resc) m_use = mt;
+        lsum *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
+      }
+      const float mb = (m_use == -INFINITY) ? 0.f : -m_use;
+      float rs = 0.f;
+#pragma unroll
+      for (int b = 0; b < NKB; ++b)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const float p = exp2_fast(fmaf(s[b][j], sl2, mb));
+          rs += p;
+          s[b][j] = p;
+        }
+      lsum += rs;
+#pragma unroll
+      for (int b = 0; b < NKB; ++b)
+#pragma unroll
+        for (int t = 0; t < T32; ++t) {
+          const Frag pf = FragFromAcc<T>::get(s[b], t);
+#pragma unroll
+          for (int db = 0; db < NDB; ++db)
+            mma(oacc[db], TransRead<T, LD>::get(vl, b, db, t, h, c), pf);
+        }
+    }
+    if (it + 1 < nt) {
+      ks.store(smem[st ^ 1][0], tid);
+      vs.store(smem[st ^ 1][1], tid);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue: lane (h, c) holds O^T columns of query qi
+  const float ltot = halves_sum(lsum);
+  const float inv = 1.f / ltot;
+  T* Og = (T*)a.o + hoff;
+  const T* dOg = a.dout ? (const T*)a.dout + hoff : nullptr;
+  float dpart = 0.f;
+  if (qi < n) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int col = 32 * db + 8 * q4 + 4 * h;
+        const float o0 = oacc[db][4 * q4 + 0] * inv, o1 = oacc[db][4 * q4 + 1] * inv;
+        const float o2 = oacc[db][4 * q4 + 2] * inv, o3 = oacc[db][4 * q4 + 3] * inv;
+        Quad<T>::store(Og + (size_t)qi * D + col, o0, o1, o2, o3);
+        if (dOg) {
+          const f32x4 g = Quad<T>::load(dOg + (size_t)qi * D + col);
+          dpart += o0 * g[0] + o1 * g[1] + o2 * g[2] + o3 * g[3];
+        }
+      }
+  }
+  const float dsum = halves_sum(dpart);
+  if (qi < n && h == 0) {
+    const size_t row = (size_t)head * n + qi;
+    a.lse[row] = (m_use + log2f(ltot)) * kLn2;
+    if (dOg) a.dvec[row] = dsum;
+  }
+}
+
+// ======================================================================
+// dK, dV: a workgroup owns BKV = 128 keys (32 per wave, held in registers as
+// B operands); Q and dO tiles of BQ = 64 queries are staged in LDS with
+// their L (pre-multiplied by log2 e) and D.
+// Per wave and 32-query block:  S = Q K^T, dP = dO V^T  (rows = queries,
+// cols = the wave's keys), P = 2^(S sl2 - L), dS = P (dP - D),
+// dV^T += dO^T P, dK^T += Q^T dS.
+// ======================================================================
+template <typename T, int D, bool CAUSAL>
+__global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
+  using E = Elem<T>;
+  using Frag = typename E::frag;
+  constexpr int BKV = 128, BQ = 64, NQB = BQ / 32, NDB = D / 32;
+  constexpr int KP = E::KP;
+  constexpr int T32 = 16 / KP;
+  using TL = Tile<T, BQ, D>;
+  constexpr int LD = TL::LD;
+  __shared__ __attribute__((aligned(16))) T smem[2][2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) float lds_l[2][BQ];
+  __shared__ __attribute__((aligned(16))) float lds_d[2][BQ];
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  int head, kt;
+  block_map(blockIdx.x, a.nblocks, a.ntiles, false, head, kt);
+  const int n = a.n;
+  const size_t hoff = (size_t)head * (size_t)a.head_stride;
+  const T* Qg = (const T*)a.q + hoff;
+  const T* Kg = (const T*)a.k + hoff;
+  const T* Vg = (const T*)a.v + hoff;
+  const T* dOg = (const T*)a.dout + hoff;
+  const float* Lg = a.lse + (size_t)head * n;
+  const float* Dg = a.dvec + (size_t)head * n;
+  const int k0 = kt * BKV, kw0 = k0 + 32 * w, kj = kw0 + c;
+
+  RowFrags<T, D> kf, vf;
+  kf.load(Kg, kj, n, h, 0u);
+  vf.load(Vg, kj, n, h, 0u);
+
+  const int q_begin = CAUSAL ? (k0 / BQ) * BQ : 0;
+  const int nt = (n - q_begin + BQ - 1) / BQ;
+
+  Stage<T, BQ, D> qs, dos;
+  float lv = 0.f, dv_ = 0.f;
+  auto load_rows = [&](int r0) {
+    qs.load(Qg, r0, n, tid, a.qflip);
+    dos.load(dOg, r0, n, tid, 0u);
+    if (tid < BQ) {
+      lv = (r0 + tid < n) ? Lg[r0 + tid] * kLog2e : 0.f;
+      dv_ = (r0 + tid < n) ? Dg[r0 + tid] : 0.f;
+    }
+  };
+  auto store_rows = [&](int st) {
+    qs.store(smem[st][0], tid);
+    dos.store(smem[st][1], tid);
+    if (tid < BQ) {
+      lds_l[st][tid] = lv;
+      lds_d[st][tid] = dv_;
+    }
+  };
+  load_rows(q_begin);
+  store_rows(0);
+  __syncthreads();
+
+  f32x16 dk[NDB], dv[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) { dk[db] = zero16(); dv[db] = zero16(); }
+  const float sl2 = a.sl2;
+
+  for (int it = 0; it < nt; ++it) {
+    const int qt0 = q_begin + it * BQ;
+    const int st = it & 1;
+    if (it + 1 < nt) load_rows(qt0 + BQ);
+    const T* ql = smem[st][0];
+    const T* dol = smem[st][1];
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) {
+      const int qb0 = qt0 + 32 * qb;
+      if (CAUSAL && qb0 + 31 < kw0) continue;  // every query of the block precedes every key
+      f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+      for (int t = 0; t < D / (2 * KP); ++t) {
+        mma(s, RowRead<T, LD>::get(ql, qb, t, h, c), kf.f[t]);
+        mma(dp, RowRead<T, LD>::get(dol, qb, t, h, c), vf.f[t]);
+      }
+      // lane (h, c): element j is query qb0 + 16h + j, key kj
+      const f32x4* lp = (const f32x4*)&lds_l[st][32 * qb + 16 * h];
+      const f32x4* dp4 = (const f32x4*)&lds_d[st][32 * qb + 16 * h];
+      const bool edge = (qb0 + 31 >= n) || (CAUSAL && qb0 < kw0 + 31);
+#pragma unroll
+      for (int j4 = 0; j4 < 4; ++j4) {
+        const f32x4 l4 = lp[j4], d4 = dp4[j4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = 4 * j4 + e;
+          float p = exp2_fast(fmaf(s[j], sl2, -l4[e]));
+          if (edge) {
+            const int q = qb0 + 16 * h + j;
+            if (q >= n || (CAUSAL && kj > q)) p = 0.f;
+          }
+          s[j] = p;
+          dp[j] = p * (dp[j] - d4[e]);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < T32; ++t) {
+        const Frag pf = FragFromAcc<T>::get(s, t);
+        const Frag sf = FragFromAcc<T>::get(dp, t);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          mma(dv[db], TransRead<T, LD>::get(dol, qb, db, t, h, c), pf);
+          mma(dk[db], TransRead<T, LD>::get(ql, qb, db, t, h, c), sf);
+        }
+      }
+    }
+    if (it + 1 < nt) store_rows(st ^ 1);
+    __syncthreads();
+  }
+
+  if (kj < n) {
+    T* dKg = (T*)a.dk + hoff;
+    T* dVg = (T*)a.dv + hoff;
+    const float sc = a.dk_scale;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int col = 32 * db + 8 * q4 + 4 * h;
+        Quad<T>::store(dKg + (size_t)kj * D + col, dk[db][4 * q4] * sc, dk[db][4 * q4 + 1] * sc,
+                       dk[db][4 * q4 + 2] * sc, dk[db][4 * q4 + 3] * sc);
+        Quad<T>::store(dVg + (size_t)kj * D + col, dv[db][4 * q4], dv[db][4 * q4 + 1],
+                       dv[db][4 * q4 + 2], dv[db][4 * q4 + 3]);
+      }
+  }
+}
+
+// ======================================================================
+// dQ: a workgroup owns BQ = 128 queries (32 per wave; Q and dO rows in
+// registers as B operands, L and D per lane); K and V tiles of BKV = 64 keys
+// are staged in LDS.
+// Per wave and 32-key block:  S^T = K Q^T, dP^T = V dO^T (rows = keys,
+// cols = the wave's queries), dS^T = P^T (dP^T - D), dQ^T += K^T dS^T.
+// ======================================================================
+template <typename T, int D, bool CAUSAL>
+__global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
+  using E = Elem<T>;
+  using Frag = typename E::frag;
+  constexpr int BQ = 128, BKV = 64, NKB = BKV / 32, NDB = D / 32;
+  constexpr int KP = E::KP;
+  constexpr int T32 = 16 / KP;
+  using TL = Tile<T, BKV, D>;
+  constexpr int LD = TL::LD;
+  __shared__ __attribute__((aligned(16))) T smem[2][2][TL::ELEMS];
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  int head, qt;
+  block_map(blockIdx.x, a.nblocks, a.ntiles, CAUSAL, head, qt);
+  const int n = a.n;
+  const size_t hoff = (size_t)head * (size_t)a.head_stride;
+  const T* Qg = (const T*)a.q + hoff;
+  const T* Kg = (const T*)a.k + hoff;
+  const T* Vg = (const T*)a.v + hoff;
+  const T* dOg = (const T*)a.dout + hoff;
+  const int q0 = qt * BQ, qw0 = q0 + 32 * w, qi = qw0 + c;
+
+  RowFrags<T, D> qf, of;
+  qf.load(Qg, qi, n, h, a.qflip);
+  of.load(dOg, qi, n, h, 0u);
+  const float lq = (qi < n) ? a.lse[(size_t)head * n + qi] * kLog2e : 0.f;
+  const float dq_ = (qi < n) ? a.dvec[(size_t)head * n + qi] : 0.f;
+
+  const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
+  const int nt = (kv_end + BKV - 1) / BKV;
+
+  Stage<T, BKV, D> ks, vs;
+  ks.load(Kg, 0, n, tid, 0u);
+  vs.load(Vg, 0, n, tid, 0u);
+  ks.store(smem[0][0], tid);
+  vs.store(smem[0][1], tid);
+  __syncthreads();
+
+  f32x16 dqa[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) dqa[db] = zero16();
+  const float sl2 = a.sl2;
+
+  for (int it = 0; it < nt; ++it) {
+    const int kv0 = it * BKV;
+    const int st = it & 1;
+    if (it + 1 < nt) {
+      ks.load(Kg, kv0 + BKV, n, tid, 0u);
+      vs.load(Vg, kv0 + BKV, n, tid, 0u);
+    }
+    const T* kl = smem[st][0];
+    const T* vl = smem[st][1];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+      const int kb0 = kv0 + 32 * kb;
+      if (CAUSAL && kb0 > qw0 + 31) continue;  // every key of the block follows every query
+      f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+      for (int t = 0; t < D / (2 * KP); ++t) {
+        mma(s, RowRead<T, LD>::get(kl, kb, t, h, c), qf.f[t]);
+        mma(dp, RowRead<T, LD>::get(vl, kb, t, h, c), of.f[t]);
+      }
+      // lane (h, c): element j is key kb0 + 16h + j, query qi
+      const bool edge = (kb0 + 31 >= n) || (CAUSAL && kb0 + 31 > qw0);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        float p = exp2_fast(fmaf(s[j], sl2, -lq));
+        if (edge) {
+          const int key = kb0 + 16 * h + j;
+          if (key >= n || (CAUSAL && key > qi)) p = 0.f;
+        }
+        dp[j] = p * (dp[j] - dq_);
+      }
+#pragma unroll
+      for (int t = 0; t < T32; ++t) {
+        const Frag sf = FragFromAcc<T>::get(dp, t);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) mma(dqa[db], TransRead<T, LD>::get(kl, kb, db, t, h, c), sf);
+      }
+    }
+    if (it + 1 < nt) {
+      ks.store(smem[st ^ 1][0], tid);
+      vs.store(smem[st ^ 1][1], tid);
+    }
+    __syncthreads();
+  }
+
+  if (qi < n) {
+    T* dQg = (T*)a.dq + hoff;
+    const float sc = a.dq_scale;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int col = 32 * db + 8 * q4 + 4 * h;
+        Quad<T>::store(dQg + (size_t)qi * D + col, dqa[db][4 * q4] * sc, dqa[db][4 * q4 + 1] * sc,
+                       dqa[db][4 * q4 + 2] * sc, dqa[db][4 * q4 + 3] * sc);
+      }
+  }
+}
+
+}  // namespace attn

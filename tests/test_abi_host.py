@@ -1,0 +1,113 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+function declared in include/attn_mi355x.h, and every validation error is
+returned before anything reaches the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "attn_mi355x.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(attn_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2609_33916_amd as pkg
+    if not os.path.exists(pkg.LIB_PATH):
+        pytest.fail("libattn_mi355x.so is not built (python -m paper_2609_33916_amd.build)")
+    return pkg.lib()
+
+
+def test_exports_every_declared_function(L):
+    names = _declared_functions()
+    assert set(names) >= {"attn_fwd", "attn_fwd_bwd", "attn_workspace_bytes", "attn_strerror"}
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_workspace_bytes(L):
+    assert L.attn_workspace_bytes(2, 32, 16384, 128) == 2 * 32 * 16384 * 4
+    assert L.attn_workspace_bytes(1, 1, 1, 32) == 4
+    assert L.attn_workspace_bytes(0, 1, 1, 32) == 0
+    assert L.attn_workspace_bytes(1, 1, -5, 32) == 0
+
+
+def test_strerror(L):
+    import paper_2609_33916_amd as pkg
+    for code in range(0, -8, -1):
+        s = pkg.attn_strerror(code)
+        assert s and "unknown" not in s
+    assert "unknown" in pkg.attn_strerror(12345)
+
+
+FAKE = 1 << 20          # aligned, never dereferenced: validation fails first
+MIS = FAKE + 2          # misaligned
+
+
+def _fwd(L, Q=FAKE, K=FAKE, V=FAKE, O=FAKE, Lse=FAKE, B=1, H=1, n=8, d=64, scale=0.125,
+         causal=0, dtype=0):
+    return L.attn_fwd(Q, K, V, O, Lse, B, H, n, d, scale, causal, dtype, None)
+
+
+def _fb(lib_, ws=FAKE, wsb=1 << 30, B=1, H=1, n=8, d=64, scale=0.125, causal=0, dtype=1, **ptr):
+    p = {k: FAKE for k in ("Q", "K", "V", "dO", "O", "L", "dQ", "dK", "dV")}
+    p.update(ptr)
+    return lib_.attn_fwd_bwd(p["Q"], p["K"], p["V"], p["dO"], p["O"], p["L"], p["dQ"], p["dK"],
+                          p["dV"], ws, wsb, B, H, n, d, scale, causal, dtype, None)
+
+
+def test_fwd_validation(L):
+    assert _fwd(L, Q=None) == -1
+    assert _fwd(L, Lse=None) == -1
+    assert _fwd(L, B=0) == -2
+    assert _fwd(L, n=0) == -2
+    assert _fwd(L, H=-1) == -2
+    assert _fwd(L, d=80) == -3
+    assert _fwd(L, d=256) == -3
+    assert _fwd(L, dtype=7) == -3
+    assert _fwd(L, scale=float("nan")) == -7
+    assert _fwd(L, scale=float("inf")) == -7
+    assert _fwd(L, causal=2) == -7
+    assert _fwd(L, V=MIS) == -4
+    assert _fwd(L, Lse=FAKE + 2) == -4
+    assert _fwd(L, n=1 << 25, d=128) == -2   # n*d beyond 32-bit indexing
+
+
+def test_fwd_bwd_validation(L):
+    for name in ("Q", "K", "V", "dO", "O", "L", "dQ", "dK", "dV"):
+        assert _fb(L, **{name: None}) == -1, name
+    assert _fb(L, ws=None) == -1
+    for name in ("Q", "K", "V", "dO", "O", "dQ", "dK", "dV"):
+        assert _fb(L, **{name: MIS}) == -4, name
+    assert _fb(L, ws=FAKE + 1) == -4
+    assert _fb(L, wsb=8 * 4 - 1) == -5
+    assert _fb(L, d=48) == -3
+    assert _fb(L, dtype=-1) == -3
+    assert _fb(L, B=0) == -2
+    assert _fb(L, scale=float("-inf")) == -7
+    assert _fb(L, causal=-1) == -7
+
+
+def test_binding_rejects_cpu_tensors():
+    import torch
+    import paper_2609_33916_amd as pkg
+    x = torch.zeros(1, 1, 8, 32)
+    with pytest.raises(ValueError):
+        pkg.attn_fwd(x, x, x)
+
+
+def test_library_source_never_allocates():
+    """No device allocation anywhere in the library: all buffers are the
+    caller's, so nothing of size n x n can exist."""
+    csrc = os.path.join(ROOT, "paper_2609_33916_amd", "csrc")
+    for fn in os.listdir(csrc):
+        text = open(os.path.join(csrc, fn)).read()
+        for call in ("hipMalloc", "hipFree", "hipMallocAsync", "hipExtMalloc", "malloc("):
+            assert call not in text, (fn, call)

@@ -20,7 +20,7 @@ from typing import Dict, Optional, Sequence
 
 import numpy as np
 
-__all__ = ["Workload", "WORKLOADS", "Inputs", "generate", "f32_to_bf16_bits",
+__all__ = ["Workload", "WORKLOADS", "Inputs", "generate", "to_torch", "f32_to_bf16_bits",
            "bf16_bits_to_f32", "round_to_bf16", "causal_pairs", "alg_flops",
            "alg_bytes"]
 
@@ -133,6 +133,19 @@ def generate(w: Workload, *, n: Optional[int] = None, B: Optional[int] = None,
             x = bf16_bits_to_f32(b)
         out[name] = x
     return Inputs(w, out["q"], out["k"], out["v"], out["do"], bits)
+
+
+def to_torch(inp: Inputs, device="cuda") -> Dict[str, "object"]:
+    """Copy the inputs to torch tensors on ``device`` in the workload's type
+    (bfloat16 from the stored bit patterns, or float32)."""
+    import torch
+    out = {}
+    for name in ("q", "k", "v", "do"):
+        if inp.workload.dtype == "bf16":
+            out[name] = torch.from_numpy(inp.bits[name].view(np.int16)).to(device).view(torch.bfloat16)
+        else:
+            out[name] = torch.from_numpy(getattr(inp, name)).to(device)
+    return out
 
 
 def causal_pairs(n: int, causal: bool) -> int:
