@@ -88,6 +88,9 @@ def main(argv=None) -> int:
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the host oracle (and with it the sampled-head error check)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="instead of the benchmark, run 5 device-to-device copies of MIB MiB "
+                         "(reference kernel of known traffic for the HBM byte counters)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -102,6 +105,15 @@ def main(argv=None) -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
+    if args.copy_calibration:
+        nbytes = args.copy_calibration << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": nbytes, "copies": 5}), flush=True)
+        return 0
     w = workloads.WORKLOADS[args.workload]
     print(f"[bench] workload {w.name}: generating seeded inputs", file=sys.stderr, flush=True)
     inp = workloads.generate(w)

@@ -27,6 +27,10 @@ HIPCC_FLAGS = [
     "-mcode-object-version=5",
     # keep the compiler from forming packed FP32 VALU instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in arch VGPRs: the softmax reads and rescales them
+    # with VALU instructions, which cannot address AGPRs; the AGPR form
+    # costs accvgpr copies every key tile
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wno-unused-command-line-argument",
 ]
 
