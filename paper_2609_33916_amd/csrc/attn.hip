@@ -164,7 +164,7 @@ static int fwd_bwd_impl(const void* Q, const void* K, const void* V, const void*
   b.head_stride = (long long)n * d;
   b.n = n;
   b.sl2 = sp.sl2;
-  b.dk_scale = sp.abs_scale;
+  b.dk_scale = scale;
   b.dq_scale = scale;
   b.qflip = sp.qflip;
 

@@ -10,8 +10,8 @@
 // v_mfma_f32_32x32x2_f32. Only the accumulator layout matters for
 // correctness: any order of k slots works as long as A and B agree.
 //
-// Tiles in LDS are row-major (contiguous along d) with a small pad, and the
-// rows of every 32-row block are stored permuted (srow below) so that
+// Tiles in LDS are row-major (contiguous along d) and the rows of every
+// 32-row block are stored permuted (srow below) so that
 //  * a "row read" (A operand = tile rows, contraction over d) has lane c read
 //    stored row c, and its accumulator row R(h, j) is logical row 16h + j;
 //    lane half h then owns 16 consecutive logical rows, which is exactly the
@@ -21,6 +21,12 @@
 //    gets 8 consecutive logical rows per lane: for bf16 with two
 //    ds_read_b64_tr_b16 (4 rows x 16 columns per 16-lane group), for float32
 //    with one 4-byte read per MFMA.
+// bf16 rows are unpadded and their 16-byte chunks XOR-swizzled (swz): LDS
+// has 64 four-byte banks; a ds_read_b128 is conflict-free when each group of
+// 16 lanes touches 16 distinct 16-byte bank slots, a ds_read_b64_tr_b16 when
+// each half-wave does. swz makes both the 16 consecutive rows of a row read
+// and the 4 rows x 4 chunks of a transposed read land on distinct slots.
+// float32 rows are padded by one element instead.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -51,7 +57,7 @@ template <typename T> struct Elem;
 template <> struct Elem<bf16> {
   using frag = bf16x8;               // one MFMA operand per lane
   static constexpr int KP = 8;       // k slots per lane per MFMA
-  static constexpr int PAD = 8;      // LDS row pad (elements)
+  static constexpr int PAD = 0;      // rows unpadded, chunks swizzled
   static constexpr int CH = 8;       // elements per 16-byte chunk
 };
 template <> struct Elem<float> {
@@ -83,6 +89,14 @@ __host__ __device__ constexpr int perm32(int r) { return ((r >> 2) & 1) * 16 + (
 __host__ __device__ constexpr int perm32_inv(int x) { return ((x >> 2) & 3) * 8 + (x >> 4) * 4 + (x & 3); }
 // stored row of logical row x (permutation inside each 32-row block)
 __host__ __device__ constexpr int srow(int x) { return (x & ~31) | perm32_inv(x & 31); }
+
+// 16-byte chunk swizzle of stored row s of a bf16 tile with D columns
+// (D/8 chunks per row, 16/(D/8) rows per 256-byte bank line).
+template <int D> __host__ __device__ constexpr int swz(int s) {
+  return D == 128 ? 4 * (s & 3) + ((s >> 2) & 3)
+       : D == 64  ? 4 * ((s >> 1) & 1) + ((s >> 2) & 3)
+                  : ((s >> 2) & 3);
+}
 
 // ------------------------------------------------------ lane-half ops --
 // Lanes c and c + 32 hold the two halves of the same accumulator column.
@@ -161,11 +175,12 @@ template <typename T, int ROWS, int D> struct Tile {
 };
 
 // Register staging of one tile: global -> registers (issued early) and
-// registers -> LDS (after the current tile's reads are done).
+// registers -> LDS (after the current tile's reads are done). Rows >= n read
+// as zeros. Used for float32 tiles (padded rows).
 template <typename T, int ROWS, int D> struct Stage {
   using TL = Tile<T, ROWS, D>;
   u32x4 r[TL::NPT];
-  __device__ __forceinline__ void load(const T* g, int row0, int n, int tid, uint32_t flip) {
+  __device__ __forceinline__ void load(const T* g, int row0, int n, int tid) {
 #pragma unroll
     for (int i = 0; i < TL::NPT; ++i) {
       const int ci = tid + 256 * i;
@@ -174,7 +189,7 @@ template <typename T, int ROWS, int D> struct Stage {
         const int row = ci / TL::CPR, cc = ci % TL::CPR;
         if (row0 + row < n) x = *(const u32x4*)(g + (size_t)(row0 + row) * D + cc * Elem<T>::CH);
       }
-      r[i] = x ^ (u32x4){flip, flip, flip, flip};
+      r[i] = x;
     }
   }
   __device__ __forceinline__ void store(T* s, int tid) const {
@@ -184,26 +199,73 @@ template <typename T, int ROWS, int D> struct Stage {
       if (TL::NCH % 256 == 0 || ci < TL::NCH) {
         const int row = ci / TL::CPR, cc = ci % TL::CPR;
         T* p = s + srow(row) * TL::LD + cc * Elem<T>::CH;
-        if constexpr (sizeof(T) == 2) {
-          *(u32x4*)p = r[i];
-        } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) ((uint32_t*)p)[e] = r[i][e];
-        }
+        for (int e = 0; e < 4; ++e) ((uint32_t*)p)[e] = r[i][e];
       }
     }
   }
 };
 
+// Global -> LDS transfer of one ROWS x D tile by a 4-wave workgroup.
+// issue() starts the copy of rows [row0, row0 + ROWS) into `lds`; commit()
+// finishes it (the caller's __syncthreads makes it visible).
+//  * bf16: global_load_lds_dwordx4, which writes each lane's 16 bytes at
+//    lane * 16 of a 1 KB wave-contiguous LDS block; every lane fetches the
+//    global chunk that belongs at its LDS slot (row permutation srow and
+//    chunk swizzle swz applied on the global side), so no registers and no
+//    LDS write instructions are spent. Rows >= n fetch row n - 1 instead
+//    (finite values; the kernels mask those rows).
+//  * float32: register staging (Stage), rows >= n as zeros.
+template <typename T, int ROWS, int D> struct TileLoader;
+template <int ROWS, int D> struct TileLoader<bf16, ROWS, D> {
+  static constexpr int C = D / 8;                        // 16-byte chunks per row
+  static constexpr int NI = ROWS * D * 2 / (4 * 1024);   // wave instructions per tile
+  static_assert(NI >= 1 && ROWS * D * 2 == NI * 4096, "tile must split into 1 KB wave blocks");
+  int off[NI];   // element offset of this lane's chunk inside the tile
+  int xr[NI];    // its logical row
+  __device__ __forceinline__ TileLoader(int w, int lane) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int L = 64 * (w * NI + j) + lane;
+      const int s = L / C, slot = L % C;
+      const int q = slot ^ swz<D>(s);
+      const int x = (s & ~31) | perm32(s & 31);
+      xr[j] = x;
+      off[j] = x * D + 8 * q;
+    }
+  }
+  __device__ __forceinline__ void issue(bf16* lds, const bf16* g, int row0, int n, int w) const {
+    const bool full = row0 + ROWS <= n;
+    const bf16* base = g + (size_t)row0 * D;
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      int o = off[j];
+      if (!full && row0 + xr[j] >= n) o -= (row0 + xr[j] - (n - 1)) * D;
+      __builtin_amdgcn_global_load_lds(base + o, (ATTN_LDS void*)(lds + 512 * (w * NI + j)), 16, 0, 0);
+    }
+  }
+  __device__ __forceinline__ void commit(bf16*) const {}
+};
+template <int ROWS, int D> struct TileLoader<float, ROWS, D> {
+  Stage<float, ROWS, D> st;
+  int tid;
+  __device__ __forceinline__ TileLoader(int w, int lane) : tid(64 * w + lane) {}
+  __device__ __forceinline__ void issue(float*, const float* g, int row0, int n, int) {
+    st.load(g, row0, n, tid);
+  }
+  __device__ __forceinline__ void commit(float* lds) const { st.store(lds, tid); }
+};
+
 // Row read: A operand = logical rows of 32-row block `rb` (stored row
 // 32*rb + c), k-step t over d.
-template <typename T, int LD> struct RowRead;
-template <int LD> struct RowRead<bf16, LD> {
+template <typename T, int D> struct RowRead;
+template <int D> struct RowRead<bf16, D> {
   __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int t, int h, int c) {
-    return *(const bf16x8*)(s + (32 * rb + c) * LD + 16 * t + 8 * h);
+    return *(const bf16x8*)(s + (32 * rb + c) * D + (((2 * t + h) ^ swz<D>(c)) * 8));
   }
 };
-template <int LD> struct RowRead<float, LD> {
+template <int D> struct RowRead<float, D> {
+  static constexpr int LD = D + Elem<float>::PAD;
   __device__ __forceinline__ static float get(const float* s, int rb, int t, int h, int c) {
     return s[(32 * rb + c) * LD + 2 * t + h];
   }
@@ -211,17 +273,19 @@ template <int LD> struct RowRead<float, LD> {
 
 // Transposed read: A operand = column 32*db + c of the tile, contraction over
 // logical rows of block rb; k-step t covers logical rows 16h + t*KP + [0, KP).
-template <typename T, int LD> struct TransRead;
-template <int LD> struct TransRead<bf16, LD> {
+template <typename T, int D> struct TransRead;
+template <int D> struct TransRead<bf16, D> {
   __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int db, int t, int h, int c) {
     // 16-lane group: source lane q = c % 16 reads stored row base + q/4 and
     // columns [32db + 16*(c/16) + 4*(q%4), +4); the transpose hands lane c
     // column 32db + c of those 4 rows.
     const int q = c & 15;
-    const int row = 32 * rb + 16 * t + 4 * h + (q >> 2);   // logical 16h+8t+k -> stored 16t+4h+k
-    const int col = 32 * db + 16 * (c >> 4) + 4 * (q & 3);
-    const bf16* p0 = s + row * LD + col;
-    const bf16* p1 = p0 + 8 * LD;                             // logical +4 -> stored +8
+    const int r0 = 32 * rb + 16 * t + 4 * h + (q >> 2);     // logical 16h+8t+k -> stored 16t+4h+k
+    const int r1 = r0 + 8;                                  // logical +4 -> stored +8
+    const int ch = 4 * db + 2 * (c >> 4) + ((q & 3) >> 1);  // 16-byte chunk of the columns
+    const int sub = (q & 1) * 4;
+    const bf16* p0 = s + r0 * D + ((ch ^ swz<D>(r0)) * 8) + sub;
+    const bf16* p1 = s + r1 * D + ((ch ^ swz<D>(r1)) * 8) + sub;
     i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p0));
     i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p1));
     // whole-register bit casts (element-wise 16-bit inserts are avoided)
@@ -229,7 +293,8 @@ template <int LD> struct TransRead<bf16, LD> {
     return __builtin_bit_cast(bf16x8, (u32x4){a[0], a[1], b[0], b[1]});
   }
 };
-template <int LD> struct TransRead<float, LD> {
+template <int D> struct TransRead<float, D> {
+  static constexpr int LD = D + Elem<float>::PAD;
   __device__ __forceinline__ static float get(const float* s, int rb, int db, int t, int h, int c) {
     return s[(32 * rb + perm32_inv(16 * h + t)) * LD + 32 * db + c];
   }

@@ -56,7 +56,7 @@ struct BwdArgs {
   int ntiles;
   int nblocks;
   float sl2;
-  float dk_scale;  // |scale|: Q is read sign-flipped when scale < 0
+  float dk_scale;  // scale (dK = s dS^T Q; K is read sign-flipped when scale < 0)
   float dq_scale;  // scale
   uint32_t qflip;
 };
@@ -76,10 +76,14 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
   constexpr int TD = D / (2 * KP);   // k-steps over d
   constexpr int T32 = 16 / KP;       // k-steps over a 32-row block
   using TL = Tile<T, BKV, D>;
-  constexpr int LD = TL::LD;
-  __shared__ __attribute__((aligned(16))) T smem[2][2][TL::ELEMS];
+  // two stages of (K, V) in distinct LDS objects: the loop is unrolled by
+  // two so every access names its stage statically, which lets the compiler
+  // see that reads of one stage never wait on the copy into the other
+  __shared__ __attribute__((aligned(16))) T stA[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) T stB[2][TL::ELEMS];
 
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   int head, qt;
   block_map(blockIdx.x, a.nblocks, a.ntiles, CAUSAL, head, qt);
   const int n = a.n;
@@ -95,11 +99,11 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
   const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
   const int nt = (kv_end + BKV - 1) / BKV;
 
-  Stage<T, BKV, D> ks, vs;
-  ks.load(Kg, 0, n, tid, 0u);
-  vs.load(Vg, 0, n, tid, 0u);
-  ks.store(smem[0][0], tid);
-  vs.store(smem[0][1], tid);
+  TileLoader<T, BKV, D> kld(w, lane), vld(w, lane);
+  kld.issue(stA[0], Kg, 0, n, w);
+  vld.issue(stA[1], Vg, 0, n, w);
+  kld.commit(stA[0]);
+  vld.commit(stA[1]);
   __syncthreads();
 
   f32x16 oacc[NDB];
@@ -108,23 +112,22 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
   float m_use = -INFINITY, lsum = 0.f;
   const float sl2 = a.sl2;
 
-  for (int it = 0; it < nt; ++it) {
+  auto step = [&](int it, T (&cur)[2][TL::ELEMS], T (&nxt)[2][TL::ELEMS]) __attribute__((always_inline)) {
     const int kv0 = it * BKV;
-    const int st = it & 1;
     if (it + 1 < nt) {
-      ks.load(Kg, kv0 + BKV, n, tid, 0u);
-      vs.load(Vg, kv0 + BKV, n, tid, 0u);
+      kld.issue(nxt[0], Kg, kv0 + BKV, n, w);
+      vld.issue(nxt[1], Vg, kv0 + BKV, n, w);
     }
     const bool active = !CAUSAL || kv0 <= qw0 + 31;
     if (active) {
-      const T* kl = smem[st][0];
-      const T* vl = smem[st][1];
+      const T* kl = cur[0];
+      const T* vl = cur[1];
       f32x16 s[NKB];
 #pragma unroll
       for (int b = 0; b < NKB; ++b) {
         s[b] = zero16();
 #pragma unroll
-        for (int t = 0; t < TD; ++t) mma(s[b], RowRead<T, LD>::get(kl, b, t, h, c), qf.f[t]);
+        for (int t = 0; t < TD; ++t) mma(s[b], RowRead<T, D>::get(kl, b, t, h, c), qf.f[t]);
       }
       // lane (h, c): s[b][j] = raw score of key kv0 + 32b + 16h + j, query qi
       const bool edge = (kv0 + BKV > n) || (CAUSAL && kv0 + BKV - 1 > qw0);
@@ -172,14 +175,18 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
           const Frag pf = FragFromAcc<T>::get(s[b], t);
 #pragma unroll
           for (int db = 0; db < NDB; ++db)
-            mma(oacc[db], TransRead<T, LD>::get(vl, b, db, t, h, c), pf);
+            mma(oacc[db], TransRead<T, D>::get(vl, b, db, t, h, c), pf);
         }
     }
     if (it + 1 < nt) {
-      ks.store(smem[st ^ 1][0], tid);
-      vs.store(smem[st ^ 1][1], tid);
+      kld.commit(nxt[0]);
+      vld.commit(nxt[1]);
     }
     __syncthreads();
+  };
+  for (int it = 0; it < nt; it += 2) {
+    step(it, stA, stB);
+    if (it + 1 < nt) step(it + 1, stB, stA);
   }
 
   // ---- epilogue: lane (h, c) holds O^T columns of query qi
@@ -227,12 +234,15 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   constexpr int KP = E::KP;
   constexpr int T32 = 16 / KP;
   using TL = Tile<T, BQ, D>;
-  constexpr int LD = TL::LD;
-  __shared__ __attribute__((aligned(16))) T smem[2][2][TL::ELEMS];
-  __shared__ __attribute__((aligned(16))) float lds_l[2][BQ];
-  __shared__ __attribute__((aligned(16))) float lds_d[2][BQ];
+  // two stages of (Q, dO) with their L and D rows, in distinct LDS objects
+  // (loop unrolled by two, as in the forward)
+  __shared__ __attribute__((aligned(16))) T stA[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) T stB[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) float ldA[2][BQ];
+  __shared__ __attribute__((aligned(16))) float ldB[2][BQ];
 
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   int head, kt;
   block_map(blockIdx.x, a.nblocks, a.ntiles, false, head, kt);
   const int n = a.n;
@@ -245,33 +255,35 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   const float* Dg = a.dvec + (size_t)head * n;
   const int k0 = kt * BKV, kw0 = k0 + 32 * w, kj = kw0 + c;
 
+  // K is read sign-flipped for a negative scale (S = |s| Q (-K)^T), so the
+  // Q tiles stay as stored and dK takes the signed scale
   RowFrags<T, D> kf, vf;
-  kf.load(Kg, kj, n, h, 0u);
+  kf.load(Kg, kj, n, h, a.qflip);
   vf.load(Vg, kj, n, h, 0u);
 
   const int q_begin = CAUSAL ? (k0 / BQ) * BQ : 0;
   const int nt = (n - q_begin + BQ - 1) / BQ;
 
-  Stage<T, BQ, D> qs, dos;
+  TileLoader<T, BQ, D> qld(w, lane), dold(w, lane);
   float lv = 0.f, dv_ = 0.f;
-  auto load_rows = [&](int r0) {
-    qs.load(Qg, r0, n, tid, a.qflip);
-    dos.load(dOg, r0, n, tid, 0u);
+  auto load_rows = [&](int r0, T (&tl)[2][TL::ELEMS]) __attribute__((always_inline)) {
+    qld.issue(tl[0], Qg, r0, n, w);
+    dold.issue(tl[1], dOg, r0, n, w);
     if (tid < BQ) {
       lv = (r0 + tid < n) ? Lg[r0 + tid] * kLog2e : 0.f;
       dv_ = (r0 + tid < n) ? Dg[r0 + tid] : 0.f;
     }
   };
-  auto store_rows = [&](int st) {
-    qs.store(smem[st][0], tid);
-    dos.store(smem[st][1], tid);
+  auto store_rows = [&](T (&tl)[2][TL::ELEMS], float (&ld)[2][BQ]) __attribute__((always_inline)) {
+    qld.commit(tl[0]);
+    dold.commit(tl[1]);
     if (tid < BQ) {
-      lds_l[st][tid] = lv;
-      lds_d[st][tid] = dv_;
+      ld[0][tid] = lv;
+      ld[1][tid] = dv_;
     }
   };
-  load_rows(q_begin);
-  store_rows(0);
+  load_rows(q_begin, stA);
+  store_rows(stA, ldA);
   __syncthreads();
 
   f32x16 dk[NDB], dv[NDB];
@@ -279,12 +291,12 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   for (int db = 0; db < NDB; ++db) { dk[db] = zero16(); dv[db] = zero16(); }
   const float sl2 = a.sl2;
 
-  for (int it = 0; it < nt; ++it) {
+  auto step = [&](int it, T (&cur)[2][TL::ELEMS], float (&lcur)[2][BQ], T (&nxt)[2][TL::ELEMS],
+                  float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
-    const int st = it & 1;
-    if (it + 1 < nt) load_rows(qt0 + BQ);
-    const T* ql = smem[st][0];
-    const T* dol = smem[st][1];
+    if (it + 1 < nt) load_rows(qt0 + BQ, nxt);
+    const T* ql = cur[0];
+    const T* dol = cur[1];
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) {
       const int qb0 = qt0 + 32 * qb;
@@ -292,12 +304,12 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
       f32x16 s = zero16(), dp = zero16();
 #pragma unroll
       for (int t = 0; t < D / (2 * KP); ++t) {
-        mma(s, RowRead<T, LD>::get(ql, qb, t, h, c), kf.f[t]);
-        mma(dp, RowRead<T, LD>::get(dol, qb, t, h, c), vf.f[t]);
+        mma(s, RowRead<T, D>::get(ql, qb, t, h, c), kf.f[t]);
+        mma(dp, RowRead<T, D>::get(dol, qb, t, h, c), vf.f[t]);
       }
       // lane (h, c): element j is query qb0 + 16h + j, key kj
-      const f32x4* lp = (const f32x4*)&lds_l[st][32 * qb + 16 * h];
-      const f32x4* dp4 = (const f32x4*)&lds_d[st][32 * qb + 16 * h];
+      const f32x4* lp = (const f32x4*)&lcur[0][32 * qb + 16 * h];
+      const f32x4* dp4 = (const f32x4*)&lcur[1][32 * qb + 16 * h];
       const bool edge = (qb0 + 31 >= n) || (CAUSAL && qb0 < kw0 + 31);
 #pragma unroll
       for (int j4 = 0; j4 < 4; ++j4) {
@@ -320,13 +332,17 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
         const Frag sf = FragFromAcc<T>::get(dp, t);
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          mma(dv[db], TransRead<T, LD>::get(dol, qb, db, t, h, c), pf);
-          mma(dk[db], TransRead<T, LD>::get(ql, qb, db, t, h, c), sf);
+          mma(dv[db], TransRead<T, D>::get(dol, qb, db, t, h, c), pf);
+          mma(dk[db], TransRead<T, D>::get(ql, qb, db, t, h, c), sf);
         }
       }
     }
-    if (it + 1 < nt) store_rows(st ^ 1);
+    if (it + 1 < nt) store_rows(nxt, lnxt);
     __syncthreads();
+  };
+  for (int it = 0; it < nt; it += 2) {
+    step(it, stA, ldA, stB, ldB);
+    if (it + 1 < nt) step(it + 1, stB, ldB, stA, ldA);
   }
 
   if (kj < n) {
@@ -361,10 +377,12 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
   constexpr int KP = E::KP;
   constexpr int T32 = 16 / KP;
   using TL = Tile<T, BKV, D>;
-  constexpr int LD = TL::LD;
-  __shared__ __attribute__((aligned(16))) T smem[2][2][TL::ELEMS];
+  // two stages of (K, V) in distinct LDS objects (loop unrolled by two)
+  __shared__ __attribute__((aligned(16))) T stA[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) T stB[2][TL::ELEMS];
 
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   int head, qt;
   block_map(blockIdx.x, a.nblocks, a.ntiles, CAUSAL, head, qt);
   const int n = a.n;
@@ -384,11 +402,11 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
   const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
   const int nt = (kv_end + BKV - 1) / BKV;
 
-  Stage<T, BKV, D> ks, vs;
-  ks.load(Kg, 0, n, tid, 0u);
-  vs.load(Vg, 0, n, tid, 0u);
-  ks.store(smem[0][0], tid);
-  vs.store(smem[0][1], tid);
+  TileLoader<T, BKV, D> kld(w, lane), vld(w, lane);
+  kld.issue(stA[0], Kg, 0, n, w);
+  vld.issue(stA[1], Vg, 0, n, w);
+  kld.commit(stA[0]);
+  vld.commit(stA[1]);
   __syncthreads();
 
   f32x16 dqa[NDB];
@@ -396,15 +414,14 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
   for (int db = 0; db < NDB; ++db) dqa[db] = zero16();
   const float sl2 = a.sl2;
 
-  for (int it = 0; it < nt; ++it) {
+  auto step = [&](int it, T (&cur)[2][TL::ELEMS], T (&nxt)[2][TL::ELEMS]) __attribute__((always_inline)) {
     const int kv0 = it * BKV;
-    const int st = it & 1;
     if (it + 1 < nt) {
-      ks.load(Kg, kv0 + BKV, n, tid, 0u);
-      vs.load(Vg, kv0 + BKV, n, tid, 0u);
+      kld.issue(nxt[0], Kg, kv0 + BKV, n, w);
+      vld.issue(nxt[1], Vg, kv0 + BKV, n, w);
     }
-    const T* kl = smem[st][0];
-    const T* vl = smem[st][1];
+    const T* kl = cur[0];
+    const T* vl = cur[1];
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
       const int kb0 = kv0 + 32 * kb;
@@ -412,8 +429,8 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
       f32x16 s = zero16(), dp = zero16();
 #pragma unroll
       for (int t = 0; t < D / (2 * KP); ++t) {
-        mma(s, RowRead<T, LD>::get(kl, kb, t, h, c), qf.f[t]);
-        mma(dp, RowRead<T, LD>::get(vl, kb, t, h, c), of.f[t]);
+        mma(s, RowRead<T, D>::get(kl, kb, t, h, c), qf.f[t]);
+        mma(dp, RowRead<T, D>::get(vl, kb, t, h, c), of.f[t]);
       }
       // lane (h, c): element j is key kb0 + 16h + j, query qi
       const bool edge = (kb0 + 31 >= n) || (CAUSAL && kb0 + 31 > qw0);
@@ -430,14 +447,18 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
       for (int t = 0; t < T32; ++t) {
         const Frag sf = FragFromAcc<T>::get(dp, t);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) mma(dqa[db], TransRead<T, LD>::get(kl, kb, db, t, h, c), sf);
+        for (int db = 0; db < NDB; ++db) mma(dqa[db], TransRead<T, D>::get(kl, kb, db, t, h, c), sf);
       }
     }
     if (it + 1 < nt) {
-      ks.store(smem[st ^ 1][0], tid);
-      vs.store(smem[st ^ 1][1], tid);
+      kld.commit(nxt[0]);
+      vld.commit(nxt[1]);
     }
     __syncthreads();
+  };
+  for (int it = 0; it < nt; it += 2) {
+    step(it, stA, stB);
+    if (it + 1 < nt) step(it + 1, stB, stA);
   }
 
   if (qi < n) {
