@@ -99,7 +99,7 @@ extern "C" {
 size_t attn_workspace_bytes(int B, int H, int n, int d) {
   (void)d;
   if (B < 1 || H < 1 || n < 1) return 0;
-  return (size_t)B * (size_t)H * (size_t)n * sizeof(float);
+  return 2 * (size_t)B * (size_t)H * (size_t)n * sizeof(float);
 }
 
 int attn_fwd(const void* Q, const void* K, const void* V, void* O, float* L,
@@ -112,7 +112,7 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O, float* L,
   const ScaleParts sp = split_scale(scale, dtype);
   attn::FwdArgs a{};
   a.q = Q; a.k = K; a.v = V; a.dout = nullptr;
-  a.o = O; a.lse = L; a.dvec = nullptr;
+  a.o = O; a.lse = L; a.dvec = nullptr; a.lse2 = nullptr;
   a.head_stride = (long long)n * d;
   a.n = n;
   a.sl2 = sp.sl2;
@@ -143,6 +143,7 @@ static int fwd_bwd_impl(const void* Q, const void* K, const void* V, const void*
   }
   const ScaleParts sp = split_scale(scale, dtype);
   float* dvec = static_cast<float*>(workspace);
+  float* lse2 = dvec + (size_t)B * H * n;
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   auto mark = [&](int i) {
@@ -151,7 +152,7 @@ static int fwd_bwd_impl(const void* Q, const void* K, const void* V, const void*
 
   attn::FwdArgs f{};
   f.q = Q; f.k = K; f.v = V; f.dout = dO;
-  f.o = O; f.lse = L; f.dvec = dvec;
+  f.o = O; f.lse = L; f.dvec = dvec; f.lse2 = lse2;
   f.head_stride = (long long)n * d;
   f.n = n;
   f.sl2 = sp.sl2;
@@ -159,7 +160,7 @@ static int fwd_bwd_impl(const void* Q, const void* K, const void* V, const void*
 
   attn::BwdArgs b{};
   b.q = Q; b.k = K; b.v = V; b.dout = dO;
-  b.lse = L; b.dvec = dvec;
+  b.lse2 = lse2; b.dvec = dvec;
   b.dq = dQ; b.dk = dK; b.dv = dV;
   b.head_stride = (long long)n * d;
   b.n = n;

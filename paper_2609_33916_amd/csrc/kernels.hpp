@@ -32,7 +32,8 @@ struct FwdArgs {
   const void* dout;   // optional: when set, D_i = sum_c dO_ic O_ic is written
   void* o;
   float* lse;
-  float* dvec;
+  float* dvec;    // optional: D rows (with dout)
+  float* lse2;    // optional: base-2 log-sum-exp rows, log2 sum_j 2^(S_ij log2 e)
   long long head_stride;  // n * d elements
   int n;
   int ntiles;    // query tiles per head
@@ -46,8 +47,8 @@ struct BwdArgs {
   const void* k;
   const void* v;
   const void* dout;
-  const float* lse;
-  const float* dvec;
+  const float* lse2;   // base-2 log-sum-exp rows written by the forward
+  const float* dvec;   // D rows written by the forward
   void* dq;
   void* dk;
   void* dv;
@@ -213,15 +214,19 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
   const float dsum = halves_sum(dpart);
   if (qi < n && h == 0) {
     const size_t row = (size_t)head * n + qi;
-    a.lse[row] = (m_use + log2f(ltot)) * kLn2;
-    if (dOg) a.dvec[row] = dsum;
+    const float l2 = m_use + log2f(ltot);
+    a.lse[row] = l2 * kLn2;
+    if (dOg) {
+      a.dvec[row] = dsum;
+      a.lse2[row] = l2;
+    }
   }
 }
 
 // ======================================================================
 // dK, dV: a workgroup owns BKV = 128 keys (32 per wave, held in registers as
 // B operands); Q and dO tiles of BQ = 64 queries are staged in LDS with
-// their L (pre-multiplied by log2 e) and D.
+// their base-2 log-sum-exp and D rows.
 // Per wave and 32-query block:  S = Q K^T, dP = dO V^T  (rows = queries,
 // cols = the wave's keys), P = 2^(S sl2 - L), dS = P (dP - D),
 // dV^T += dO^T P, dK^T += Q^T dS.
@@ -251,7 +256,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   const T* Kg = (const T*)a.k + hoff;
   const T* Vg = (const T*)a.v + hoff;
   const T* dOg = (const T*)a.dout + hoff;
-  const float* Lg = a.lse + (size_t)head * n;
+  const float* Lg = a.lse2 + (size_t)head * n;
   const float* Dg = a.dvec + (size_t)head * n;
   const int k0 = kt * BKV, kw0 = k0 + 32 * w, kj = kw0 + c;
 
@@ -265,25 +270,22 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   const int nt = (n - q_begin + BQ - 1) / BQ;
 
   TileLoader<T, BQ, D> qld(w, lane), dold(w, lane);
-  float lv = 0.f, dv_ = 0.f;
-  auto load_rows = [&](int r0, T (&tl)[2][TL::ELEMS]) __attribute__((always_inline)) {
+  // base-2 LSE and D rows of the tile: one 4-byte-per-lane LDS DMA each
+  // (waves 0 and 1); rows >= n fetch row n - 1 (masked by the kernel)
+  auto load_rows = [&](int r0, T (&tl)[2][TL::ELEMS], float (&ld)[2][BQ]) __attribute__((always_inline)) {
     qld.issue(tl[0], Qg, r0, n, w);
     dold.issue(tl[1], dOg, r0, n, w);
-    if (tid < BQ) {
-      lv = (r0 + tid < n) ? Lg[r0 + tid] * kLog2e : 0.f;
-      dv_ = (r0 + tid < n) ? Dg[r0 + tid] : 0.f;
+    if (w < 2) {
+      const int r = min(r0 + lane, n - 1);
+      __builtin_amdgcn_global_load_lds((w == 0 ? Lg : Dg) + r, (ATTN_LDS void*)(ld[w]), 4, 0, 0);
     }
   };
-  auto store_rows = [&](T (&tl)[2][TL::ELEMS], float (&ld)[2][BQ]) __attribute__((always_inline)) {
+  auto store_rows = [&](T (&tl)[2][TL::ELEMS]) __attribute__((always_inline)) {
     qld.commit(tl[0]);
     dold.commit(tl[1]);
-    if (tid < BQ) {
-      ld[0][tid] = lv;
-      ld[1][tid] = dv_;
-    }
   };
-  load_rows(q_begin, stA);
-  store_rows(stA, ldA);
+  load_rows(q_begin, stA, ldA);
+  store_rows(stA);
   __syncthreads();
 
   f32x16 dk[NDB], dv[NDB];
@@ -294,7 +296,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   auto step = [&](int it, T (&cur)[2][TL::ELEMS], float (&lcur)[2][BQ], T (&nxt)[2][TL::ELEMS],
                   float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
-    if (it + 1 < nt) load_rows(qt0 + BQ, nxt);
+    if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt);
     const T* ql = cur[0];
     const T* dol = cur[1];
 #pragma unroll
@@ -337,7 +339,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
         }
       }
     }
-    if (it + 1 < nt) store_rows(nxt, lnxt);
+    if (it + 1 < nt) store_rows(nxt);
     __syncthreads();
   };
   for (int it = 0; it < nt; it += 2) {
@@ -396,7 +398,7 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
   RowFrags<T, D> qf, of;
   qf.load(Qg, qi, n, h, a.qflip);
   of.load(dOg, qi, n, h, 0u);
-  const float lq = (qi < n) ? a.lse[(size_t)head * n + qi] * kLog2e : 0.f;
+  const float lq = (qi < n) ? a.lse2[(size_t)head * n + qi] : 0.f;
   const float dq_ = (qi < n) ? a.dvec[(size_t)head * n + qi] : 0.f;
 
   const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;

@@ -33,8 +33,8 @@ def test_exports_every_declared_function(L):
 
 
 def test_workspace_bytes(L):
-    assert L.attn_workspace_bytes(2, 32, 16384, 128) == 2 * 32 * 16384 * 4
-    assert L.attn_workspace_bytes(1, 1, 1, 32) == 4
+    assert L.attn_workspace_bytes(2, 32, 16384, 128) == 2 * 2 * 32 * 16384 * 4
+    assert L.attn_workspace_bytes(1, 1, 1, 32) == 8
     assert L.attn_workspace_bytes(0, 1, 1, 32) == 0
     assert L.attn_workspace_bytes(1, 1, -5, 32) == 0
 
@@ -87,7 +87,7 @@ def test_fwd_bwd_validation(L):
     for name in ("Q", "K", "V", "dO", "O", "dQ", "dK", "dV"):
         assert _fb(L, **{name: MIS}) == -4, name
     assert _fb(L, ws=FAKE + 1) == -4
-    assert _fb(L, wsb=8 * 4 - 1) == -5
+    assert _fb(L, wsb=2 * 8 * 4 - 1) == -5
     assert _fb(L, d=48) == -3
     assert _fb(L, dtype=-1) == -3
     assert _fb(L, B=0) == -2
