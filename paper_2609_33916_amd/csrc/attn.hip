@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdint>
 #include <limits>
+#include <type_traits>
 
 #include "attn_mi355x.h"
 #include "kernels.hpp"
@@ -58,11 +59,24 @@ void launch_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
   hipLaunchKernelGGL((attn::fwd_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
 }
 
+// dK/dV: bf16 uses the 16-key-per-wave kernel (8 waves, 128 keys per
+// workgroup, 64-query tiles); float32 the 32-key-per-wave kernel.
+constexpr int kDkv16Waves = 8;
+constexpr int kDkv16BQ = 64;
+
 template <typename T, int D, bool CAUSAL>
 void launch_dkdv(attn::BwdArgs a, int heads, hipStream_t st) {
-  a.ntiles = (a.n + kDkvBKV - 1) / kDkvBKV;
-  a.nblocks = heads * a.ntiles;
-  hipLaunchKernelGGL((attn::dkdv_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
+  if constexpr (std::is_same<T, bf16>::value) {
+    constexpr int bkv = 16 * kDkv16Waves;
+    a.ntiles = (a.n + bkv - 1) / bkv;
+    a.nblocks = heads * a.ntiles;
+    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, kDkv16Waves, kDkv16BQ>), dim3(a.nblocks),
+                       dim3(64 * kDkv16Waves), 0, st, a);
+  } else {
+    a.ntiles = (a.n + kDkvBKV - 1) / kDkvBKV;
+    a.nblocks = heads * a.ntiles;
+    hipLaunchKernelGGL((attn::dkdv_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
+  }
 }
 
 template <typename T, int D, bool CAUSAL>

@@ -300,6 +300,96 @@ template <int D> struct TransRead<float, D> {
   }
 };
 
+// ------------------------------------------------- 16x16x32 variant --
+// v_mfma_f32_16x16x32_bf16 (lane l, group g = l / 16, c = l % 16):
+//   A: row c, k slots 8g + [0, 8); B: col c, same slots; accumulator: col c,
+//   rows 4g + [0, 4).
+// Chaining two 16-row accumulator blocks (rows 4g + j and 16 + 4g + j) into
+// one operand gives every lane group the k slots of 8 rows that come as two
+// runs of 4 consecutive rows, which is exactly what two ds_read_b64_tr_b16
+// return. Tiles for this variant keep rows in natural order; their 16-byte
+// chunks are swizzled with swz16 so that 16 consecutive rows of one chunk
+// (row reads) and 8 consecutive rows of two adjacent chunks (transposed
+// reads, per half-wave) each land on distinct bank slots.
+__device__ __forceinline__ void mma16(f32x4& acc, const bf16x8& a, const bf16x8& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+}
+
+template <int D> __host__ __device__ constexpr int swz16(int s) {
+  return D == 128 ? 2 * (s & 7) + ((s >> 3) & 1)
+       : D == 64  ? 2 * ((s >> 1) & 3) + ((s >> 3) & 1)
+                  : 2 * ((s >> 2) & 1) + ((s >> 3) & 1);
+}
+
+// Global -> LDS DMA of a ROWS x D bf16 tile (natural row order, swz16
+// chunks) by NW waves: 1 KB wave instructions, instruction i issued by wave
+// i % NW. Rows >= n fetch row n - 1.
+template <int ROWS, int D, int NW> struct TileLoader16 {
+  static constexpr int C = D / 8;
+  static constexpr int TI = ROWS * D * 2 / 1024;          // wave instructions per tile
+  static constexpr int NI = (TI + NW - 1) / NW;            // per wave (upper bound)
+  static_assert(ROWS * D * 2 == TI * 1024, "tile must split into 1 KB wave blocks");
+  int off[NI];
+  int xr[NI];
+  __device__ __forceinline__ TileLoader16(int w, int lane) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int L = 64 * (w + NW * j) + lane;   // 16-byte chunk slot in the tile
+      const int s = L / C, slot = L % C;
+      xr[j] = s;
+      off[j] = s * D + 8 * (slot ^ swz16<D>(s));
+    }
+  }
+  __device__ __forceinline__ void issue(bf16* lds, const bf16* g, int row0, int n, int w) const {
+    const bool full = row0 + ROWS <= n;
+    const bf16* base = g + (size_t)row0 * D;
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      if (TI % NW == 0 || w + NW * j < TI) {
+        int o = off[j];
+        if (!full && row0 + xr[j] >= n) o -= (row0 + xr[j] - (n - 1)) * D;
+        __builtin_amdgcn_global_load_lds(base + o, (ATTN_LDS void*)(lds + 512 * (w + NW * j)), 16, 0, 0);
+      }
+    }
+  }
+};
+
+// Row read (16-wide): A operand = tile rows 16*rb + c, k-step t covers
+// d in [32t, 32t + 32), lane group g takes d in [32t + 8g, +8).
+template <int D>
+__device__ __forceinline__ bf16x8 row_read16(const bf16* s, int rb, int t, int g, int c) {
+  const int r = 16 * rb + c;
+  return *(const bf16x8*)(s + r * D + 8 * ((4 * t + g) ^ swz16<D>(r)));
+}
+
+// Transposed read (16-wide): A operand = columns 16*db + c, k slots = rows
+// r0 + 4g + [0, 4) and r0 + 16 + 4g + [0, 4).
+template <int D>
+__device__ __forceinline__ bf16x8 tr_read16(const bf16* s, int r0, int db, int g, int c) {
+  const int ra = r0 + 4 * g + (c >> 2);
+  const int rb2 = ra + 16;
+  const int ch = 2 * db + ((c & 3) >> 1);
+  const int sub = (c & 1) * 4;
+  const bf16* p0 = s + ra * D + 8 * (ch ^ swz16<D>(ra)) + sub;
+  const bf16* p1 = s + rb2 * D + 8 * (ch ^ swz16<D>(rb2)) + sub;
+  i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p0));
+  i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p1));
+  const u32x2 x = __builtin_bit_cast(u32x2, lo), y = __builtin_bit_cast(u32x2, hi);
+  return __builtin_bit_cast(bf16x8, (u32x4){x[0], x[1], y[0], y[1]});
+}
+
+// bf16 operand from two 16-row accumulator blocks (slots 0-3 from `a`,
+// 4-7 from `b`).
+__device__ __forceinline__ bf16x8 frag16(const f32x4& a, const f32x4& b) {
+  bf16x8 f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[i] = (bf16)a[i];
+    f[4 + i] = (bf16)b[i];
+  }
+  return f;
+}
+
 // ------------------------------------------------------ output stores --
 // Accumulator of a transposed product: lane (h, c) holds, for j-quad a,
 // 4 consecutive columns 32*db + 8a + 4h + [0, 4) of its row.

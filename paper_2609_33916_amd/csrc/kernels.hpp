@@ -365,6 +365,146 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 }
 
 // ======================================================================
+// dK, dV for bf16 on v_mfma_f32_16x16x32_bf16: a workgroup of NW waves owns
+// 16 * NW keys, 16 per wave (K and V rows of the wave's keys as B operands in
+// registers, dK^T and dV^T accumulators of 16 columns), so a wave needs about
+// half the registers of the 32-key form and two waves share each SIMD: one
+// wave's softmax VALU work overlaps the other's matrix products. Q and dO
+// tiles of BQ queries (with their base-2 LSE and D rows) are staged in LDS;
+// every 32 queries form one k step of the dV/dK products:
+//   S = Q K^T, dP = dO V^T          (two 16-query blocks each)
+//   P = 2^(S sl2 - L), dS = P (dP - D)
+//   dV^T += dO^T P, dK^T += Q^T dS  (contraction over the 32 queries)
+// ======================================================================
+template <int D, bool CAUSAL, int NW, int BQ>
+__global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
+  constexpr int BKV = 16 * NW, NPB = BQ / 32, TD = D / 32, NDB = D / 16;
+  __shared__ __attribute__((aligned(16))) bf16 stA[2][BQ * D];
+  __shared__ __attribute__((aligned(16))) bf16 stB[2][BQ * D];
+  __shared__ __attribute__((aligned(16))) float ldA[2][BQ];
+  __shared__ __attribute__((aligned(16))) float ldB[2][BQ];
+
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int head, kt;
+  block_map(blockIdx.x, a.nblocks, a.ntiles, false, head, kt);
+  const int n = a.n;
+  const size_t hoff = (size_t)head * (size_t)a.head_stride;
+  const bf16* Qg = (const bf16*)a.q + hoff;
+  const bf16* Kg = (const bf16*)a.k + hoff;
+  const bf16* Vg = (const bf16*)a.v + hoff;
+  const bf16* dOg = (const bf16*)a.dout + hoff;
+  const float* Lg = a.lse2 + (size_t)head * n;
+  const float* Dg = a.dvec + (size_t)head * n;
+  const int k0 = kt * BKV, kw0 = k0 + 16 * w, kj = kw0 + c;
+
+  // B operands: row kj of K (sign-flipped for a negative scale) and of V;
+  // k-step t holds d in [32t + 8g, +8)
+  bf16x8 kf[TD], vf[TD];
+#pragma unroll
+  for (int t = 0; t < TD; ++t) {
+    u32x4 x = {0u, 0u, 0u, 0u}, y = {0u, 0u, 0u, 0u};
+    if (kj < n) {
+      x = *(const u32x4*)(Kg + (size_t)kj * D + 32 * t + 8 * g);
+      y = *(const u32x4*)(Vg + (size_t)kj * D + 32 * t + 8 * g);
+    }
+    x ^= (u32x4){a.qflip, a.qflip, a.qflip, a.qflip};
+    kf[t] = __builtin_bit_cast(bf16x8, x);
+    vf[t] = __builtin_bit_cast(bf16x8, y);
+  }
+
+  const int q_begin = CAUSAL ? (k0 / BQ) * BQ : 0;
+  const int nt = (n - q_begin + BQ - 1) / BQ;
+
+  TileLoader16<BQ, D, NW> tld(w, lane);
+  auto load_rows = [&](int r0, bf16 (&tl)[2][BQ * D], float (&lr)[2][BQ]) __attribute__((always_inline)) {
+    tld.issue(tl[0], Qg, r0, n, w);
+    tld.issue(tl[1], dOg, r0, n, w);
+    if (w < 2) {
+      const int r = min(r0 + lane, n - 1);
+      if (lane < BQ)
+        __builtin_amdgcn_global_load_lds((w == 0 ? Lg : Dg) + r, (ATTN_LDS void*)(lr[w]), 4, 0, 0);
+    }
+  };
+  load_rows(q_begin, stA, ldA);
+  __syncthreads();
+
+  f32x4 dk[NDB], dv[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+    dk[db] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    dv[db] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  }
+  const float sl2 = a.sl2;
+
+  auto step = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&nxt)[2][BQ * D],
+                  float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
+    const int qt0 = q_begin + it * BQ;
+    if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt);
+    const bf16* ql = cur[0];
+    const bf16* dol = cur[1];
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      const int qp0 = qt0 + 32 * pb;
+      if (CAUSAL && qp0 + 31 < kw0) continue;  // every query of the block precedes every key
+      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = sa, pa = sa, pc = sa;
+#pragma unroll
+      for (int t = 0; t < TD; ++t) {
+        mma16(sa, row_read16<D>(ql, 2 * pb, t, g, c), kf[t]);
+        mma16(sb, row_read16<D>(ql, 2 * pb + 1, t, g, c), kf[t]);
+        mma16(pa, row_read16<D>(dol, 2 * pb, t, g, c), vf[t]);
+        mma16(pc, row_read16<D>(dol, 2 * pb + 1, t, g, c), vf[t]);
+      }
+      // lane (g, c): sa[j] / sb[j] = S of query qp0 + 4g + j / qp0 + 16 + 4g + j, key kj
+      const f32x4 la = *(const f32x4*)&lcur[0][32 * pb + 4 * g];
+      const f32x4 lb = *(const f32x4*)&lcur[0][32 * pb + 16 + 4 * g];
+      const f32x4 da = *(const f32x4*)&lcur[1][32 * pb + 4 * g];
+      const f32x4 dd = *(const f32x4*)&lcur[1][32 * pb + 16 + 4 * g];
+      const bool edge = (qp0 + 31 >= n) || (CAUSAL && qp0 < kw0 + 15);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float p0 = exp2_fast(fmaf(sa[j], sl2, -la[j]));
+        float p1 = exp2_fast(fmaf(sb[j], sl2, -lb[j]));
+        if (edge) {
+          const int q0 = qp0 + 4 * g + j, q1 = q0 + 16;
+          if (q0 >= n || (CAUSAL && kj > q0)) p0 = 0.f;
+          if (q1 >= n || (CAUSAL && kj > q1)) p1 = 0.f;
+        }
+        sa[j] = p0;
+        sb[j] = p1;
+        pa[j] = p0 * (pa[j] - da[j]);
+        pc[j] = p1 * (pc[j] - dd[j]);
+      }
+      const bf16x8 pf = frag16(sa, sb);
+      const bf16x8 sf = frag16(pa, pc);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        mma16(dv[db], tr_read16<D>(dol, 32 * pb, db, g, c), pf);
+        mma16(dk[db], tr_read16<D>(ql, 32 * pb, db, g, c), sf);
+      }
+    }
+    __syncthreads();
+  };
+  for (int it = 0; it < nt; it += 2) {
+    step(it, stA, ldA, stB, ldB);
+    if (it + 1 < nt) step(it + 1, stB, ldB, stA, ldA);
+  }
+
+  if (kj < n) {
+    bf16* dKg = (bf16*)a.dk + hoff;
+    bf16* dVg = (bf16*)a.dv + hoff;
+    const float sc = a.dk_scale;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const int col = 16 * db + 4 * g;
+      Quad<bf16>::store(dKg + (size_t)kj * D + col, dk[db][0] * sc, dk[db][1] * sc, dk[db][2] * sc,
+                        dk[db][3] * sc);
+      Quad<bf16>::store(dVg + (size_t)kj * D + col, dv[db][0], dv[db][1], dv[db][2], dv[db][3]);
+    }
+  }
+}
+
+// ======================================================================
 // dQ: a workgroup owns BQ = 128 queries (32 per wave; Q and dO rows in
 // registers as B operands, L and D per lane); K and V tiles of BKV = 64 keys
 // are staged in LDS.
