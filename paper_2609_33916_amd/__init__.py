@@ -25,7 +25,10 @@ import torch  # loads the process's HIP runtime before the library
 __all__ = ["attn_fwd", "attn_fwd_bwd", "attn_fwd_bwd_timed", "attn_workspace_bytes", "attn_strerror",
            "AttnError", "lib", "LIB_PATH", "ATTN_BF16", "ATTN_F32"]
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libattn_mi355x.so")
+# ATTN_MI355X_LIB may name another build of the same library (A/B comparison
+# of compiler settings); by default the in-tree build is loaded.
+LIB_PATH = os.environ.get("ATTN_MI355X_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libattn_mi355x.so")
 ATTN_BF16 = 0
 ATTN_F32 = 1
 

@@ -22,10 +22,12 @@
 //    ds_read_b64_tr_b16 (4 rows x 16 columns per 16-lane group), for float32
 //    with one 4-byte read per MFMA.
 // bf16 rows are unpadded and their 16-byte chunks XOR-swizzled (swz): LDS
-// has 64 four-byte banks; a ds_read_b128 is conflict-free when each group of
-// 16 lanes touches 16 distinct 16-byte bank slots, a ds_read_b64_tr_b16 when
-// each half-wave does. swz makes both the 16 consecutive rows of a row read
-// and the 4 rows x 4 chunks of a transposed read land on distinct slots.
+// has 64 four-byte banks (16 slots of 16 bytes per 256-byte line); each
+// ds_read_b128 pass serves 16 lanes and each ds_read_b64(_tr_b16) pass a
+// half-wave, and a pass is conflict-free when its lanes touch distinct
+// slots (see swz16 for which lanes share a pass). swz makes the rows of a
+// row read and the 4 rows x 4 chunks of a transposed read land on distinct
+// slots.
 // float32 rows are padded by one element instead.
 #pragma once
 
@@ -66,6 +68,13 @@ template <> struct Elem<float> {
   static constexpr int PAD = 1;
   static constexpr int CH = 4;
 };
+
+// ----------------------------------------------------- schedule hints --
+// Instruction classes for __builtin_amdgcn_sched_group_barrier: the
+// pipelined loops ask the scheduler to alternate matrix products with the
+// LDS reads that feed later products and with independent VALU work.
+enum : int { kSchedVALU = 0x2, kSchedMFMA = 0x8, kSchedDSRead = 0x100 };
+#define ATTN_SCHED(mask, count) __builtin_amdgcn_sched_group_barrier((mask), (count), 0)
 
 // ------------------------------------------------------------------ MFMA --
 __device__ __forceinline__ void mma(f32x16& acc, const bf16x8& a, const bf16x8& b) {
@@ -315,10 +324,15 @@ __device__ __forceinline__ void mma16(f32x4& acc, const bf16x8& a, const bf16x8&
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
 }
 
+// On gfx950 a ds_read_b64 (also _tr_b16) serves each half-wave in one pass;
+// a ds_read_b128 serves the 16 lanes that share bit 5 and the parity of
+// bits 2, 3, 4 of the lane index (measured with single lane pairs), so the
+// row read of this variant puts lanes (g, c) with g0 = parity(c2, c3) + const
+// together; these swizzles are conflict-free for both patterns.
 template <int D> __host__ __device__ constexpr int swz16(int s) {
-  return D == 128 ? 2 * (s & 7) + ((s >> 3) & 1)
-       : D == 64  ? 2 * ((s >> 1) & 3) + ((s >> 3) & 1)
-                  : 2 * ((s >> 2) & 1) + ((s >> 3) & 1);
+  return D == 128 ? 2 * (s & 7)
+       : D == 64  ? 2 * ((s >> 1) & 3)
+                  : 2 * ((s >> 2) & 1);
 }
 
 // Global -> LDS DMA of a ROWS x D bf16 tile (natural row order, swz16

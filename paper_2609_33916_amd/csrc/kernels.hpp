@@ -21,6 +21,8 @@
 // natural log on output. A negative scale is folded into Q's sign.
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace attn {
@@ -437,53 +439,121 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   }
   const float sl2 = a.sl2;
 
-  auto step = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&nxt)[2][BQ * D],
-                  float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
+  // S and dP of pair block pb (queries 32pb + [0, 32) of the staged tile)
+  auto sdp = [&](const bf16* ql, const bf16* dol, int pb, f32x4 (&sv)[2], f32x4 (&pv)[2])
+      __attribute__((always_inline)) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      sv[x] = (f32x4){0.f, 0.f, 0.f, 0.f};
+      pv[x] = sv[x];
+    }
+#pragma unroll
+    for (int t = 0; t < TD; ++t)
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        mma16(sv[x], row_read16<D>(ql, 2 * pb + x, t, g, c), kf[t]);
+        mma16(pv[x], row_read16<D>(dol, 2 * pb + x, t, g, c), vf[t]);
+      }
+  };
+  // P = 2^(S sl2 - L), dS = P (dP - D) as bf16 operands; with MASK, queries
+  // >= n and (causal) queries before key kj get P = 0
+  auto softmax = [&](const float (&lr)[2][BQ], int pb, int qp0, f32x4 (&sv)[2], f32x4 (&pv)[2],
+                     bf16x8& pf, bf16x8& sf, auto mask) __attribute__((always_inline)) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      const f32x4 l4 = *(const f32x4*)&lr[0][32 * pb + 16 * x + 4 * g];
+      const f32x4 d4 = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float p = exp2_fast(fmaf(sv[x][j], sl2, -l4[j]));
+        if constexpr (decltype(mask)::value) {
+          const int q = qp0 + 16 * x + 4 * g + j;
+          if (q >= n || (CAUSAL && kj > q)) p = 0.f;
+        }
+        sv[x][j] = p;
+        pv[x][j] = p * (pv[x][j] - d4[j]);
+      }
+    }
+    pf = frag16(sv[0], sv[1]);
+    sf = frag16(pv[0], pv[1]);
+  };
+  auto dvdk = [&](const bf16* ql, const bf16* dol, int pb, const bf16x8& pf, const bf16x8& sf)
+      __attribute__((always_inline)) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      mma16(dv[db], tr_read16<D>(dol, 32 * pb, db, g, c), pf);
+      mma16(dk[db], tr_read16<D>(ql, 32 * pb, db, g, c), sf);
+    }
+  };
+
+  // Tiles that touch the diagonal or the end of the sequence: pair blocks
+  // one after another, with masks.
+  auto step_edge = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&nxt)[2][BQ * D],
+                       float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt);
-    const bf16* ql = cur[0];
-    const bf16* dol = cur[1];
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
       const int qp0 = qt0 + 32 * pb;
       if (CAUSAL && qp0 + 31 < kw0) continue;  // every query of the block precedes every key
-      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = sa, pa = sa, pc = sa;
+      f32x4 sv[2], pv[2];
+      bf16x8 pf, sf;
+      sdp(cur[0], cur[1], pb, sv, pv);
+      softmax(lcur, pb, qp0, sv, pv, pf, sf, std::true_type{});
+      dvdk(cur[0], cur[1], pb, pf, sf);
+    }
+    __syncthreads();
+  };
+  // Interior tiles (every query sees every key of the workgroup, all rows
+  // valid): software-pipelined, the S/dP products of pair block pb + 1 are
+  // issued next to the exponentials of pair block pb, whose dV/dK products
+  // follow.
+  auto step_inner = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&nxt)[2][BQ * D],
+                        float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
+    const int qt0 = q_begin + it * BQ;
+    if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt);
+    f32x4 sv[2][2], pv[2][2];
+    sdp(cur[0], cur[1], 0, sv[0], pv[0]);
 #pragma unroll
-      for (int t = 0; t < TD; ++t) {
-        mma16(sa, row_read16<D>(ql, 2 * pb, t, g, c), kf[t]);
-        mma16(sb, row_read16<D>(ql, 2 * pb + 1, t, g, c), kf[t]);
-        mma16(pa, row_read16<D>(dol, 2 * pb, t, g, c), vf[t]);
-        mma16(pc, row_read16<D>(dol, 2 * pb + 1, t, g, c), vf[t]);
-      }
-      // lane (g, c): sa[j] / sb[j] = S of query qp0 + 4g + j / qp0 + 16 + 4g + j, key kj
-      const f32x4 la = *(const f32x4*)&lcur[0][32 * pb + 4 * g];
-      const f32x4 lb = *(const f32x4*)&lcur[0][32 * pb + 16 + 4 * g];
-      const f32x4 da = *(const f32x4*)&lcur[1][32 * pb + 4 * g];
-      const f32x4 dd = *(const f32x4*)&lcur[1][32 * pb + 16 + 4 * g];
-      const bool edge = (qp0 + 31 >= n) || (CAUSAL && qp0 < kw0 + 15);
+    for (int pb = 0; pb < NPB; ++pb) {
+      if (pb + 1 < NPB) sdp(cur[0], cur[1], pb + 1, sv[(pb + 1) & 1], pv[(pb + 1) & 1]);
+      bf16x8 pf, sf;
+      softmax(lcur, pb, qt0 + 32 * pb, sv[pb & 1], pv[pb & 1], pf, sf, std::false_type{});
+      dvdk(cur[0], cur[1], pb, pf, sf);
+    }
+    // schedule: S/dP of block 0 with its row reads running ahead; then per
+    // block pb, its exponentials next to the next block's S/dP products and
+    // next to its own dV/dK products (whose transposed reads run ahead)
+    ATTN_SCHED(kSchedDSRead, 4);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float p0 = exp2_fast(fmaf(sa[j], sl2, -la[j]));
-        float p1 = exp2_fast(fmaf(sb[j], sl2, -lb[j]));
-        if (edge) {
-          const int q0 = qp0 + 4 * g + j, q1 = q0 + 16;
-          if (q0 >= n || (CAUSAL && kj > q0)) p0 = 0.f;
-          if (q1 >= n || (CAUSAL && kj > q1)) p1 = 0.f;
+    for (int i = 0; i < 4 * TD; ++i) { ATTN_SCHED(kSchedMFMA, 1); ATTN_SCHED(kSchedDSRead, 1); }
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      if (pb + 1 < NPB) {
+#pragma unroll
+        for (int i = 0; i < 4 * TD; ++i) {
+          ATTN_SCHED(kSchedMFMA, 1);
+          ATTN_SCHED(kSchedDSRead, 1);
+          ATTN_SCHED(kSchedVALU, 2);
         }
-        sa[j] = p0;
-        sb[j] = p1;
-        pa[j] = p0 * (pa[j] - da[j]);
-        pc[j] = p1 * (pc[j] - dd[j]);
       }
-      const bf16x8 pf = frag16(sa, sb);
-      const bf16x8 sf = frag16(pa, pc);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        mma16(dv[db], tr_read16<D>(dol, 32 * pb, db, g, c), pf);
-        mma16(dk[db], tr_read16<D>(ql, 32 * pb, db, g, c), sf);
+      for (int i = 0; i < 2 * NDB; ++i) {
+        ATTN_SCHED(kSchedMFMA, 1);
+        ATTN_SCHED(kSchedDSRead, 2);
+        ATTN_SCHED(kSchedVALU, 2);
       }
     }
     __syncthreads();
+  };
+  auto step = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&nxt)[2][BQ * D],
+                  float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
+    const int qt0 = q_begin + it * BQ;
+    // the pipelined form pays off at d = 128; at smaller d a pair block has
+    // too few products to hide the exponentials behind
+    const bool inner = D == 128 && qt0 + BQ <= n && (!CAUSAL || qt0 >= k0 + BKV - 1);
+    if (inner) step_inner(it, cur, lcur, nxt, lnxt);
+    else step_edge(it, cur, lcur, nxt, lnxt);
   };
   for (int it = 0; it < nt; it += 2) {
     step(it, stA, ldA, stB, ldB);
