@@ -86,6 +86,19 @@ int attn_fwd_bwd(const void* Q, const void* K, const void* V, const void* dO,
                  int B, int H, int n, int d, float scale, int causal, int dtype,
                  void* stream);
 
+/* Backward only (Paper II's "Algorithm 1" reads the forward's results back
+ * from memory; here only the O(n) row statistics are): dQ, dK, dV from Q, K,
+ * V, the forward's O and L, and dO. A pre-pass computes D_i = sum_c dO_ic O_ic
+ * from the given O (in its stored precision) and the base-2 L into the
+ * workspace (attn_workspace_bytes(B,H,n,d) bytes); then the dK/dV and dQ
+ * kernels of attn_fwd_bwd run unchanged. O and L must be the forward's outputs
+ * for the same Q, K, V, scale and mask. */
+int attn_bwd(const void* Q, const void* K, const void* V, const void* O, const float* L,
+             const void* dO, void* dQ, void* dK, void* dV,
+             void* workspace, size_t workspace_bytes,
+             int B, int H, int n, int d, float scale, int causal, int dtype,
+             void* stream);
+
 /* attn_fwd_bwd with per-kernel timing: when `events` is not NULL it must
  * point to 4 hipEvent_t created by the caller; events[0] is recorded on
  * `stream` before the forward kernel, events[1] after it, events[2] after the

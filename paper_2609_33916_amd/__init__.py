@@ -22,7 +22,7 @@ from typing import Optional, Tuple
 
 import torch  # loads the process's HIP runtime before the library
 
-__all__ = ["attn_fwd", "attn_fwd_bwd", "attn_fwd_bwd_timed", "attn_workspace_bytes", "attn_strerror",
+__all__ = ["attn_fwd", "attn_fwd_bwd", "attn_fwd_bwd_timed", "attn_bwd", "attn_workspace_bytes", "attn_strerror",
            "AttnError", "lib", "LIB_PATH", "ATTN_BF16", "ATTN_F32"]
 
 # ATTN_MI355X_LIB may name another build of the same library (A/B comparison
@@ -60,6 +60,8 @@ def lib() -> ctypes.CDLL:
     L.attn_fwd_bwd_timed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                      i, i, i, i, f, i, i, vp, ctypes.POINTER(vp)]
     L.attn_fwd_bwd_timed.restype = i
+    L.attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, f, i, i, vp]
+    L.attn_bwd.restype = i
     L.attn_strerror.argtypes = [i]
     L.attn_strerror.restype = ctypes.c_char_p
     _lib = L
@@ -129,6 +131,31 @@ def attn_fwd_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, do: torch.Te
     ``out`` may supply preallocated (O, L, dQ, dK, dV) and ``workspace`` a
     uint8 GPU tensor of at least attn_workspace_bytes(B, H, n, d) bytes."""
     return _fwd_bwd(q, k, v, do, scale, causal, out, workspace, None)
+
+
+def attn_bwd(q, k, v, o, lse, do, scale: Optional[float] = None, causal: bool = False,
+             out=None, workspace=None):
+    """Backward only from the forward's O and L: returns (dQ, dK, dV)."""
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, n, d]")
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("do", do)):
+        _check(name, t, q)
+    B, H, n, d = q.shape
+    if lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, n) or not lse.is_contiguous() \
+            or lse.device != q.device:
+        raise ValueError("lse must be contiguous float32 [B, H, n] on q's device")
+    dQ, dK, dV = (torch.empty_like(q) for _ in range(3)) if out is None else out
+    wsb = attn_workspace_bytes(B, H, n, d)
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    rc = lib().attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                        do.data_ptr(), dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
+                        workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                        B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
+                        _stream(q.device))
+    if rc != 0:
+        raise AttnError(rc, "attn_bwd")
+    return dQ, dK, dV
 
 
 def attn_fwd_bwd_timed(q, k, v, do, events, scale: Optional[float] = None, causal: bool = False,

@@ -87,6 +87,14 @@ void launch_dq(attn::BwdArgs a, int heads, hipStream_t st) {
 }
 
 template <typename T, int D, bool C>
+struct PrepL {
+  static void run(attn::PrepArgs a, int, hipStream_t st) {
+    constexpr int rpb = 256 / (D / attn::Elem<T>::CH);
+    const long long blocks = (a.rows + rpb - 1) / rpb;
+    hipLaunchKernelGGL((attn::bwd_prep_kernel<T, D>), dim3((unsigned)blocks), dim3(256), 0, st, a);
+  }
+};
+template <typename T, int D, bool C>
 struct FwdL { static void run(attn::FwdArgs a, int heads, hipStream_t st) { launch_fwd<T, D, C>(a, heads, st); } };
 template <typename T, int D, bool C>
 struct DkvL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { launch_dkdv<T, D, C>(a, heads, st); } };
@@ -199,6 +207,47 @@ int attn_fwd_bwd(const void* Q, const void* K, const void* V, const void* dO,
                  int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
   return fwd_bwd_impl(Q, K, V, dO, O, L, dQ, dK, dV, workspace, workspace_bytes,
                       B, H, n, d, scale, causal, dtype, stream, nullptr);
+}
+
+int attn_bwd(const void* Q, const void* K, const void* V, const void* O, const float* L,
+             const void* dO, void* dQ, void* dK, void* dV,
+             void* workspace, size_t workspace_bytes,
+             int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
+  if (!Q || !K || !V || !O || !L || !dO || !dQ || !dK || !dV || !workspace) return ATTN_E_NULL;
+  int rc = check_common(B, H, n, d, scale, causal, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) ||
+      !aligned(dO, 16) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) ||
+      !aligned(L, 4) || !aligned(workspace, 4))
+    return ATTN_E_ALIGN;
+  if (workspace_bytes < attn_workspace_bytes(B, H, n, d)) return ATTN_E_WORKSPACE;
+  const ScaleParts sp = split_scale(scale, dtype);
+  float* dvec = static_cast<float*>(workspace);
+  float* lse2 = dvec + (size_t)B * H * n;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+
+  attn::PrepArgs p{};
+  p.o = O; p.dout = dO; p.lse = L; p.dvec = dvec; p.lse2 = lse2;
+  p.rows = (long long)B * H * n;
+  run_dispatch<PrepL>(dtype, d, causal, p, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+
+  attn::BwdArgs b{};
+  b.q = Q; b.k = K; b.v = V; b.dout = dO;
+  b.lse2 = lse2; b.dvec = dvec;
+  b.dq = dQ; b.dk = dK; b.dv = dV;
+  b.head_stride = (long long)n * d;
+  b.n = n;
+  b.sl2 = sp.sl2;
+  b.dk_scale = scale;
+  b.dq_scale = scale;
+  b.qflip = sp.qflip;
+  run_dispatch<DkvL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  run_dispatch<DqL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  return ATTN_OK;
 }
 
 int attn_fwd_bwd_timed(const void* Q, const void* K, const void* V, const void* dO,

@@ -65,6 +65,53 @@ struct BwdArgs {
 };
 
 // ======================================================================
+// Backward pre-pass (attn_bwd): D_i = sum_c dO_ic O_ic and the base-2 log-sum-
+// exp L_i log2(e) for every row, from a stored O and L. HBM-bound: each row
+// is read once as 16-byte chunks, a group of D/CH lanes per row reduces with
+// cross-lane adds.
+// ======================================================================
+struct PrepArgs {
+  const void* o;
+  const void* dout;
+  const float* lse;
+  float* dvec;
+  float* lse2;
+  long long rows;   // B * H * n
+};
+
+template <typename T, int D>
+__global__ void __launch_bounds__(256) bwd_prep_kernel(const PrepArgs a) {
+  constexpr int CH = Elem<T>::CH;      // elements per 16-byte chunk
+  constexpr int G = D / CH;            // lanes per row (4..32)
+  constexpr int RPB = 256 / G;         // rows per block
+  const int tid = threadIdx.x;
+  const long long row = (long long)blockIdx.x * RPB + tid / G;
+  const int part = tid % G;
+  float acc = 0.f;
+  if (row < a.rows) {
+    const u32x4 x = *(const u32x4*)((const T*)a.o + row * D + part * CH);
+    const u32x4 y = *(const u32x4*)((const T*)a.dout + row * D + part * CH);
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc += __uint_as_float(x[e] << 16) * __uint_as_float(y[e] << 16);
+        acc += __uint_as_float(x[e] & 0xffff0000u) * __uint_as_float(y[e] & 0xffff0000u);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc += __uint_as_float(x[e]) * __uint_as_float(y[e]);
+    }
+  }
+  // reduce over the G lanes of the row (G divides 64, groups are aligned)
+#pragma unroll
+  for (int off = G / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (row < a.rows && part == 0) {
+    a.dvec[row] = acc;
+    a.lse2[row] = a.lse[row] * kLog2e;
+  }
+}
+
+// ======================================================================
 // Forward: a workgroup owns BQ = 128 queries (32 per wave); K and V tiles of
 // BKV = 64 keys are staged in LDS (double-buffered through registers).
 // Per wave and key tile:  S^T = K Q^T (rows = keys, cols = the wave's 32

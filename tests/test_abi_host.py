@@ -95,6 +95,19 @@ def test_fwd_bwd_validation(L):
     assert _fb(L, causal=-1) == -7
 
 
+def test_bwd_validation(L):
+    def call(**kw):
+        p = {k: FAKE for k in ("Q", "K", "V", "O", "L", "dO", "dQ", "dK", "dV", "ws")}
+        p.update(kw)
+        return L.attn_bwd(p["Q"], p["K"], p["V"], p["O"], p["L"], p["dO"], p["dQ"], p["dK"],
+                          p["dV"], p["ws"], kw.get("wsb", 1 << 30), 1, 1, 8, 64, 0.125, 0, 0, None)
+    for name in ("Q", "K", "V", "O", "L", "dO", "dQ", "dK", "dV", "ws"):
+        assert call(**{name: None}) == -1, name
+    for name in ("Q", "K", "V", "O", "dO", "dQ", "dK", "dV"):
+        assert call(**{name: MIS}) == -4, name
+    assert call(wsb=1) == -5
+
+
 def test_binding_rejects_cpu_tensors():
     import torch
     import paper_2609_33916_amd as pkg

@@ -116,3 +116,42 @@ def test_repeat_calls_are_bitwise_identical():
         again = run_fwd_bwd(dev, w.scale, True)
         for k in OUTPUTS:
             assert torch.equal(first[k], again[k]), k
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("n,d", [(1, 64), (77, 32), (333, 64), (1000, 128)])
+def test_backward_entry_point(dtype, causal, n, d):
+    """attn_bwd from the oracle's O (stored in the input dtype) and L."""
+    import torch
+    import paper_2609_33916_amd as lib
+    w = workloads.Workload(f"bwd_{dtype}", 2, 2, n, d, dtype, causal, 1.0, 1.0,
+                           1.0 if dtype == "f32" else 0.1, 300 + n + d)
+    inp = workloads.generate(w)
+    dev = to_gpu(inp)
+    ref = oracle.attention(inp.q, inp.k, inp.v, inp.do, w.scale, causal)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    O = torch.from_numpy(ref["O"].astype(np.float32)).to("cuda").to(tdt)
+    L = torch.from_numpy(ref["L"].astype(np.float32)).to("cuda")
+    dQ, dK, dV = lib.attn_bwd(dev["q"], dev["k"], dev["v"], O, L, dev["do"], scale=w.scale,
+                              causal=causal)
+    torch.cuda.synchronize()
+    errs = compare({"dQ": to_host64(dQ), "dK": to_host64(dK), "dV": to_host64(dV)}, ref,
+                   keys=("dQ", "dK", "dV"))
+    _check(errs, dtype, f"attn_bwd n={n} d={d} {dtype} causal={causal}")
+
+
+def test_backward_entry_point_matches_fused_call():
+    import torch
+    import paper_2609_33916_amd as lib
+    w = workloads.WORKLOADS["b8h16_n4096_d64_bf16_causal"]
+    inp = workloads.generate(w, B=1, H=4)
+    dev = to_gpu(inp)
+    O, L, dQ, dK, dV = lib.attn_fwd_bwd(dev["q"], dev["k"], dev["v"], dev["do"], scale=w.scale,
+                                        causal=True)
+    bQ, bK, bV = lib.attn_bwd(dev["q"], dev["k"], dev["v"], O, L, dev["do"], scale=w.scale,
+                              causal=True)
+    torch.cuda.synchronize()
+    for a, b in ((dQ, bQ), (dK, bK), (dV, bV)):
+        diff = (a.float() - b.float()).abs().max().item() / a.float().abs().max().item()
+        assert diff <= 1e-2, diff
