@@ -95,12 +95,62 @@ def cpu_threads() -> int:
     return len(os.sched_getaffinity(0))
 
 
+def bench_entry(args, w, inp, dev, out, ws, hip, torch, attn) -> int:
+    """Time attn_fwd (4 d flops per pair) or attn_bwd (10 d per pair) alone;
+    the roofline entry then covers the whole call."""
+    q, k, v, do = dev["q"], dev["k"], dev["v"], dev["do"]
+    O, L, dQ, dK, dV = out
+    B, H, n, d = q.shape
+    # attn_bwd consumes a real forward result
+    attn.attn_fwd(q, k, v, scale=w.scale, causal=w.causal, out=(O, L))
+    if args.mode == "fwd":
+        call = lambda: attn.attn_fwd(q, k, v, scale=w.scale, causal=w.causal, out=(O, L))
+        per_pair = 4
+    else:
+        call = lambda: attn.attn_bwd(q, k, v, O, L, do, scale=w.scale, causal=w.causal,
+                                     out=(dQ, dK, dV), workspace=ws)
+        per_pair = 10
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = hip.create(), hip.create()
+    stream = torch.cuda.current_stream().cuda_stream
+    hip.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    t0 = time.perf_counter()
+    hip.hip.hipEventRecord(e0, stream)
+    for _ in range(args.steps):
+        call()
+    hip.hip.hipEventRecord(e1, stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    dev_ms = hip.elapsed_ms(e0, e1) / args.steps
+    flops = per_pair * d * workloads.causal_pairs(n, w.causal) * B * H
+    value = flops / (wall_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.dtype]
+    achieved = flops / (dev_ms * 1e-3) / 1e12
+    print(json.dumps({
+        "metric": f"attention {'forward' if args.mode == 'fwd' else 'backward'} TFLOP/s (1 GPU)",
+        "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(wall_ms, 4), "device_ms_per_step": round(dev_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic", "pct_of_peak": round(100 * value / peak, 2),
+        "config": {"workload": w.name, "entry": "attn_" + args.mode, "B": B, "H": H, "n": n, "d": d,
+                   "causal": w.causal, "alg_flops": flops},
+        "roofline": {"kernel": "attn_" + args.mode + " (whole call)", "bound": "mfma",
+                     "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None},
+    }), flush=True)
+    return 0
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--mode", default="fwd_bwd", choices=("fwd_bwd", "fwd", "bwd"),
+                    help="entry point timed: attn_fwd_bwd (default), attn_fwd, or attn_bwd")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the host oracle (and with it the sampled-head error check)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -142,6 +192,8 @@ def main(argv=None) -> int:
     out = (O, L, dQ, dK, dV)
 
     hip = HipEvents()
+    if args.mode != "fwd_bwd":
+        return bench_entry(args, w, inp, dev, out, ws, hip, torch, attn)
     evs = [[hip.create() for _ in range(4)] for _ in range(args.steps)]
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
