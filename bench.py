@@ -1,6 +1,8 @@
 """Benchmark of the fused attention forward+backward pass on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py --mode fwd|bwd      attn_fwd or attn_bwd alone
+    python bench.py --mode naive        fused versus the naive materialising path
 
 One step is one attn_fwd_bwd call (forward, dK/dV and dQ kernels) over the
 whole workload, inputs resident in HBM before timing starts. Prints ONE JSON
@@ -143,14 +145,127 @@ def bench_entry(args, w, inp, dev, out, ws, hip, torch, attn) -> int:
     return 0
 
 
+def _time_calls(call, steps, warmup, hip, torch):
+    """(device ms, wall ms) per call over `steps` back-to-back calls."""
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = hip.create(), hip.create()
+    stream = torch.cuda.current_stream().cuda_stream
+    hip.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    t0 = time.perf_counter()
+    hip.hip.hipEventRecord(e0, stream)
+    for _ in range(steps):
+        call()
+    hip.hip.hipEventRecord(e1, stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    dev_ms = hip.elapsed_ms(e0, e1) / steps
+    hip.destroy(e0)
+    hip.destroy(e1)
+    return dev_ms, wall
+
+
+def mat_written_elems(n: int, causal: bool) -> int:
+    """Elements of P the materialising forward writes per head: every 64-key
+    tile a 32-query block visits, for the block's rows < n (its forward
+    workgroups own 128 queries; under the causal mask a block visits the
+    tiles that start at or before its last query)."""
+    total = 0
+    for qw0 in range(0, n, 32):
+        rows = min(32, n - qw0)
+        q0 = qw0 // 128 * 128
+        kv_end = min(n, q0 + 128) if causal else n
+        tiles = sum(1 for kv0 in range(0, kv_end, 64) if not causal or kv0 <= qw0 + 31)
+        total += rows * 64 * tiles
+    return total
+
+
+def bench_naive(args, w, inp, dev, out, ws, hip, torch, attn) -> int:
+    """The paper's central comparison on this GPU: the fused path (attn_fwd_bwd)
+    against the naive path that stores the attention matrix, timed as forward
+    alone + backward alone (attn_mat_fwd, attn_mat_bwd) and as one call."""
+    q, k, v, do = dev["q"], dev["k"], dev["v"], dev["do"]
+    O, L, dQ, dK, dV = out
+    B, H, n, d = q.shape
+    e = 2 if w.dtype == "bf16" else 4
+    P = torch.empty((B, H, n, attn.attn_mat_lda(n)), dtype=q.dtype, device=q.device)
+    O2, L2 = torch.empty_like(O), torch.empty_like(L)
+    g2 = tuple(torch.empty_like(q) for _ in range(3))
+    fused = lambda: attn.attn_fwd_bwd(q, k, v, do, scale=w.scale, causal=w.causal, out=out, workspace=ws)
+    mfwd = lambda: attn.attn_mat_fwd(q, k, v, scale=w.scale, causal=w.causal, out=(O2, L2), P=P)
+    mbwd = lambda: attn.attn_mat_bwd(q, k, v, O2, do, P, scale=w.scale, causal=w.causal, out=g2,
+                                     workspace=ws)
+    mboth = lambda: attn.attn_mat_fwd_bwd(q, k, v, do, scale=w.scale, causal=w.causal,
+                                          out=(O2, L2) + g2, P=P, workspace=ws)
+    print("[bench] naive: fused, naive forward, naive backward, naive one call", file=sys.stderr, flush=True)
+    t = {}
+    t["fused"] = _time_calls(fused, args.steps, args.warmup, hip, torch)
+    t["naive_fwd"] = _time_calls(mfwd, args.steps, args.warmup, hip, torch)
+    t["naive_bwd"] = _time_calls(mbwd, args.steps, args.warmup, hip, torch)
+    t["naive_call"] = _time_calls(mboth, args.steps, args.warmup, hip, torch)
+    naive_ms = t["naive_fwd"][0] + t["naive_bwd"][0]
+    f_alg = workloads.alg_flops(B, H, n, d, w.causal)
+    heads = B * H
+    p_elems = mat_written_elems(n, w.causal) * heads
+    # naive forward element count (Table tab:paper1-dram's model): read Q, K, V
+    # once, write P (the tiles written) and O once, plus the float32 L rows
+    model = {"read": 3 * heads * n * d * e, "write": p_elems * e + heads * n * d * e + 4 * heads * n}
+    rec = {
+        "metric": "fused / naive device time, attention fwd+bwd (1 GPU)",
+        "value": round(t["fused"][0] / naive_ms, 4), "unit": "ratio", "higher_is_better": False,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "H": H, "n": n, "d": d, "causal": w.causal},
+        "fused_ms": round(t["fused"][0], 4),
+        "fused_tflops": round(f_alg / (t["fused"][0] * 1e-3) / 1e12, 2),
+        "naive_fwd_ms": round(t["naive_fwd"][0], 4),
+        "naive_bwd_ms": round(t["naive_bwd"][0], 4),
+        "naive_ms": round(naive_ms, 4),
+        "naive_one_call_ms": round(t["naive_call"][0], 4),
+        "naive_tflops": round(f_alg / (naive_ms * 1e-3) / 1e12, 2),
+        "fused_over_naive_one_call": round(t["fused"][0] / t["naive_call"][0], 4),
+        "p_stored_bytes": p_elems * e,
+        "naive_fwd_hbm_model_bytes": model,
+        "naive_fwd_model_gbs": round((model["read"] + model["write"]) / (t["naive_fwd"][0] * 1e-3) / 1e9, 1),
+    }
+    tr = measured_traffic_kernel(w.name, "mat_fwd_kernel", prefix="hbm_traffic_naive")
+    if tr is not None:
+        rec["naive_fwd_hbm_measured_bytes"] = tr
+        rec["naive_fwd_measured_over_model"] = {
+            "read": round(tr["fetch_bytes"] / model["read"], 3),
+            "write": round(tr["write_bytes"] / model["write"], 3),
+            "total": round((tr["fetch_bytes"] + tr["write_bytes"]) / (model["read"] + model["write"]), 3)}
+    if not args.no_cpu_baseline:
+        import oracle
+        torch.cuda.synchronize()
+        b, h = B - 1, H // 2
+        ref = oracle.attention_head(inp.q[b, h], inp.k[b, h], inp.v[b, h], inp.do[b, h], w.scale, w.causal)
+        got = {"O": O2[b, h], "L": L2[b, h], "dQ": g2[0][b, h], "dK": g2[1][b, h], "dV": g2[2][b, h]}
+        rec["naive_max_rel_err"] = {key: float(f"{oracle.max_rel_err(x.float().cpu().numpy(), ref[key]):.3e}")
+                                    for key, x in got.items()}
+        rec["naive_max_rel_err_sample"] = f"head ({b}, {h}) vs float64 oracle"
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+def measured_traffic_kernel(workload: str, kernel: str, prefix: str = "hbm_traffic"):
+    """fetch/write bytes per launch of `kernel` from a committed summary, or None."""
+    from paper_2609_33916_amd import profiling
+    rec = profiling.read_traffic(os.path.join(ROOT, "profiles", f"{prefix}_{workload}.md"))
+    if not rec or rec.get("source_hash") != profiling.source_hash():
+        return None
+    return rec["kernels"].get(kernel)
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(workloads.WORKLOADS))
-    ap.add_argument("--mode", default="fwd_bwd", choices=("fwd_bwd", "fwd", "bwd"),
-                    help="entry point timed: attn_fwd_bwd (default), attn_fwd, or attn_bwd")
+    ap.add_argument("--mode", default="fwd_bwd", choices=("fwd_bwd", "fwd", "bwd", "naive"),
+                    help="entry point timed: attn_fwd_bwd (default), attn_fwd, attn_bwd, or the "
+                         "fused path against the naive materialising path")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the host oracle (and with it the sampled-head error check)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -192,6 +307,8 @@ def main(argv=None) -> int:
     out = (O, L, dQ, dK, dV)
 
     hip = HipEvents()
+    if args.mode == "naive":
+        return bench_naive(args, w, inp, dev, out, ws, hip, torch, attn)
     if args.mode != "fwd_bwd":
         return bench_entry(args, w, inp, dev, out, ws, hip, torch, attn)
     evs = [[hip.create() for _ in range(4)] for _ in range(args.steps)]

@@ -6,11 +6,14 @@
  * naive path materialises the n x n attention matrix A and reads it back,
  * the fused path consumes A as soon as it is produced (Fig. fig:concept,
  * section sec:dnf-onf-machines; Paper II, sections sec:paper2-cpu and
- * sec:paper2-gv-fix). This library is the fused path: no n x n buffer is ever
- * allocated or written, and each output element has a single writer (the
- * race-free restructuring of Paper II, section sec:paper2-crash, and the
- * per-key-column gradient pass of section sec:paper2-gv-fix), so no global
- * atomics are issued.
+ * sec:paper2-gv-fix). The attn_fwd / attn_fwd_bwd / attn_bwd entry points are
+ * the fused path: no n x n buffer is ever allocated or written, and each
+ * output element has a single writer (the race-free restructuring of Paper
+ * II, section sec:paper2-crash, and the per-key-column gradient pass of
+ * section sec:paper2-gv-fix), so no global atomics are issued. The attn_mat_*
+ * entry points are the naive path on the same kernels' tiling, kept for the
+ * paper's fused-versus-naive comparison: the forward writes A, the backward
+ * reads it instead of recomputing it.
  *
  * Mathematics (per batch b and head h; s = scale):
  *   S = s Q K^T, masked to -inf where key j > query i when causal
@@ -60,7 +63,8 @@ enum {
   ATTN_E_SHAPE = -2,       /* B, H or n < 1, or the problem is too large to index */
   ATTN_E_UNSUPPORTED = -3, /* d not in {32, 64, 128}, or unknown dtype */
   ATTN_E_ALIGN = -4,       /* a tensor is not 16-byte aligned (L/workspace: 4-byte) */
-  ATTN_E_WORKSPACE = -5,   /* workspace_bytes < attn_workspace_bytes(B, H, n, d) */
+  ATTN_E_WORKSPACE = -5,   /* workspace_bytes < attn_workspace_bytes(B, H, n, d), or
+                              p_bytes < attn_mat_bytes(B, H, n, dtype) */
   ATTN_E_HIP = -6,         /* the HIP runtime rejected a kernel launch */
   ATTN_E_ARG = -7          /* scale not finite, or causal not 0/1 */
 };
@@ -111,6 +115,52 @@ int attn_fwd_bwd_timed(const void* Q, const void* K, const void* V, const void* 
                        void* workspace, size_t workspace_bytes,
                        int B, int H, int n, int d, float scale, int causal, int dtype,
                        void* stream, void* const* events);
+
+/* ---- Naive (materialising) path --------------------------------------
+ * The realisation the paper compares the fused one against: the forward
+ * stores the attention matrix A = P (Table tab:paper1-dram counts it as the
+ * n x n array written next to Out) and the backward reads P back instead of
+ * recomputing it (Paper II, section sec:paper2-cpu, "Algorithm 1").
+ *
+ * P layout: [B, H, n, lda] in `dtype`, lda = n rounded up to a multiple of
+ * 128; element (b, h, i, j) = P_ij for query i < n and key j < n. The forward
+ * writes, per 32-query block, every 64-key tile that holds a key the block
+ * sees (all tiles without a mask; under the causal mask the tiles up to the
+ * diagonal), with zeros where masked; entries it does not write are left
+ * untouched and never used. The caller allocates P (attn_mat_bytes
+ * bytes, 16-byte aligned) and owns it.
+ * Sizes: n <= 1048576 (ATTN_E_SHAPE otherwise). */
+
+/* Bytes of the P buffer: B*H*n*lda*sizeof(dtype); 0 for invalid sizes. */
+size_t attn_mat_bytes(int B, int H, int n, int dtype);
+
+/* Naive forward: O, L and P from Q, K, V. Two sweeps over the key tiles per
+ * query block: the first computes each row's log-sum-exp, the second writes
+ * the normalised P and accumulates O = P V (for bf16, from P as stored). */
+int attn_mat_fwd(const void* Q, const void* K, const void* V, void* O, float* L,
+                 void* P, size_t p_bytes,
+                 int B, int H, int n, int d, float scale, int causal, int dtype,
+                 void* stream);
+
+/* Naive backward: dQ, dK, dV from Q, K, V, the forward's O and P, and dO.
+ * A pre-pass computes D_i = sum_c dO_ic O_ic into the workspace
+ * (attn_workspace_bytes(B,H,n,d) bytes); dV = P^T dO and dS = P (dP - D)
+ * then use the stored P. P and O must be attn_mat_fwd's outputs for the same
+ * Q, K, V, scale and mask. */
+int attn_mat_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const void* P, size_t p_bytes, void* dQ, void* dK, void* dV,
+                 void* workspace, size_t workspace_bytes,
+                 int B, int H, int n, int d, float scale, int causal, int dtype,
+                 void* stream);
+
+/* Naive forward then backward in one call (the forward also computes D from
+ * dO, as attn_fwd_bwd does): same outputs as attn_fwd_bwd, plus P. */
+int attn_mat_fwd_bwd(const void* Q, const void* K, const void* V, const void* dO,
+                     void* O, float* L, void* P, size_t p_bytes,
+                     void* dQ, void* dK, void* dV,
+                     void* workspace, size_t workspace_bytes,
+                     int B, int H, int n, int d, float scale, int causal, int dtype,
+                     void* stream);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* attn_strerror(int code);

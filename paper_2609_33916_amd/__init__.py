@@ -7,6 +7,8 @@ memory and the current stream.
 
     O, L = attn_fwd(q, k, v, scale, causal)
     O, L, dQ, dK, dV = attn_fwd_bwd(q, k, v, do, scale, causal)
+    O, L, P = attn_mat_fwd(q, k, v, scale, causal)          # naive path: P stored
+    dQ, dK, dV = attn_mat_bwd(q, k, v, O, do, P, scale, causal)
 
 Tensors are contiguous [B, H, n, d] on one GPU, all bfloat16 or all float32;
 L is float32 [B, H, n] (natural-log log-sum-exp of the scaled, masked scores).
@@ -23,6 +25,7 @@ from typing import Optional, Tuple
 import torch  # loads the process's HIP runtime before the library
 
 __all__ = ["attn_fwd", "attn_fwd_bwd", "attn_fwd_bwd_timed", "attn_bwd", "attn_workspace_bytes", "attn_strerror",
+           "attn_mat_bytes", "attn_mat_lda", "attn_mat_fwd", "attn_mat_bwd", "attn_mat_fwd_bwd",
            "AttnError", "lib", "LIB_PATH", "ATTN_BF16", "ATTN_F32"]
 
 # ATTN_MI355X_LIB may name another build of the same library (A/B comparison
@@ -62,6 +65,15 @@ def lib() -> ctypes.CDLL:
     L.attn_fwd_bwd_timed.restype = i
     L.attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, f, i, i, vp]
     L.attn_bwd.restype = i
+    L.attn_mat_bytes.argtypes = [i, i, i, i]
+    L.attn_mat_bytes.restype = sz
+    L.attn_mat_fwd.argtypes = [vp, vp, vp, vp, vp, vp, sz, i, i, i, i, f, i, i, vp]
+    L.attn_mat_fwd.restype = i
+    L.attn_mat_bwd.argtypes = [vp, vp, vp, vp, vp, vp, sz, vp, vp, vp, vp, sz, i, i, i, i, f, i, i, vp]
+    L.attn_mat_bwd.restype = i
+    L.attn_mat_fwd_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, sz, vp, vp, vp, vp, sz,
+                                   i, i, i, i, f, i, i, vp]
+    L.attn_mat_fwd_bwd.restype = i
     L.attn_strerror.argtypes = [i]
     L.attn_strerror.restype = ctypes.c_char_p
     _lib = L
@@ -196,3 +208,97 @@ def _fwd_bwd(q, k, v, do, scale, causal, out, workspace, events):
     if rc != 0:
         raise AttnError(rc, where)
     return O, L, dQ, dK, dV
+
+
+# ---------------------------------------------------------------- naive path --
+def attn_mat_lda(n: int) -> int:
+    """Row stride (elements) of the stored attention matrix: n rounded up to 128."""
+    return (n + 127) // 128 * 128
+
+
+def attn_mat_bytes(B: int, H: int, n: int, dtype: torch.dtype) -> int:
+    code = ATTN_BF16 if dtype == torch.bfloat16 else ATTN_F32
+    return int(lib().attn_mat_bytes(B, H, n, code))
+
+
+def _mat_buffer(q: torch.Tensor, P: Optional[torch.Tensor]) -> torch.Tensor:
+    B, H, n, _ = q.shape
+    if P is None:
+        return torch.empty((B, H, n, attn_mat_lda(n)), dtype=q.dtype, device=q.device)
+    if P.dtype != q.dtype or not P.is_contiguous() or P.device != q.device:
+        raise ValueError("P must be a contiguous tensor of q's dtype on q's device")
+    return P
+
+
+def attn_mat_fwd(q, k, v, scale: Optional[float] = None, causal: bool = False, out=None, P=None):
+    """Naive forward: returns (O, L, P); P is [B, H, n, attn_mat_lda(n)] with
+    P[..., i, j] the attention probability of key j < n for query i."""
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, n, d]")
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(name, t, q)
+    B, H, n, d = q.shape
+    if out is None:
+        O = torch.empty_like(q)
+        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
+    else:
+        O, L = out
+    P = _mat_buffer(q, P)
+    rc = lib().attn_mat_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), O.data_ptr(), L.data_ptr(),
+                            P.data_ptr(), P.numel() * P.element_size(),
+                            B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
+                            _stream(q.device))
+    if rc != 0:
+        raise AttnError(rc, "attn_mat_fwd")
+    return O, L, P
+
+
+def attn_mat_bwd(q, k, v, o, do, P, scale: Optional[float] = None, causal: bool = False,
+                 out=None, workspace=None):
+    """Naive backward from the stored P: returns (dQ, dK, dV)."""
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, n, d]")
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("do", do)):
+        _check(name, t, q)
+    B, H, n, d = q.shape
+    P = _mat_buffer(q, P)
+    dQ, dK, dV = (torch.empty_like(q) for _ in range(3)) if out is None else out
+    if workspace is None:
+        workspace = torch.empty(max(attn_workspace_bytes(B, H, n, d), 1), dtype=torch.uint8, device=q.device)
+    rc = lib().attn_mat_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), do.data_ptr(),
+                            P.data_ptr(), P.numel() * P.element_size(),
+                            dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
+                            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                            B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
+                            _stream(q.device))
+    if rc != 0:
+        raise AttnError(rc, "attn_mat_bwd")
+    return dQ, dK, dV
+
+
+def attn_mat_fwd_bwd(q, k, v, do, scale: Optional[float] = None, causal: bool = False,
+                     out=None, P=None, workspace=None):
+    """Naive forward+backward: returns (O, L, dQ, dK, dV, P)."""
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, n, d]")
+    for name, t in (("q", q), ("k", k), ("v", v), ("do", do)):
+        _check(name, t, q)
+    B, H, n, d = q.shape
+    if out is None:
+        O = torch.empty_like(q)
+        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
+        dQ, dK, dV = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    else:
+        O, L, dQ, dK, dV = out
+    P = _mat_buffer(q, P)
+    if workspace is None:
+        workspace = torch.empty(max(attn_workspace_bytes(B, H, n, d), 1), dtype=torch.uint8, device=q.device)
+    rc = lib().attn_mat_fwd_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
+                                O.data_ptr(), L.data_ptr(), P.data_ptr(), P.numel() * P.element_size(),
+                                dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
+                                workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
+                                _stream(q.device))
+    if rc != 0:
+        raise AttnError(rc, "attn_mat_fwd_bwd")
+    return O, L, dQ, dK, dV, P

@@ -64,26 +64,33 @@ void launch_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
 constexpr int kDkv16Waves = 8;
 constexpr int kDkv16BQ = 64;
 
-template <typename T, int D, bool CAUSAL>
+template <typename T, int D, bool CAUSAL, bool MAT = false>
 void launch_dkdv(attn::BwdArgs a, int heads, hipStream_t st) {
   if constexpr (std::is_same<T, bf16>::value) {
     constexpr int bkv = 16 * kDkv16Waves;
     a.ntiles = (a.n + bkv - 1) / bkv;
     a.nblocks = heads * a.ntiles;
-    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, kDkv16Waves, kDkv16BQ>), dim3(a.nblocks),
+    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, kDkv16Waves, kDkv16BQ, MAT>), dim3(a.nblocks),
                        dim3(64 * kDkv16Waves), 0, st, a);
   } else {
     a.ntiles = (a.n + kDkvBKV - 1) / kDkvBKV;
     a.nblocks = heads * a.ntiles;
-    hipLaunchKernelGGL((attn::dkdv_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((attn::dkdv_kernel<T, D, CAUSAL, MAT>), dim3(a.nblocks), dim3(256), 0, st, a);
   }
 }
 
-template <typename T, int D, bool CAUSAL>
+template <typename T, int D, bool CAUSAL, bool MAT = false>
 void launch_dq(attn::BwdArgs a, int heads, hipStream_t st) {
   a.ntiles = (a.n + kFwdBQ - 1) / kFwdBQ;
   a.nblocks = heads * a.ntiles;
-  hipLaunchKernelGGL((attn::dq_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((attn::dq_kernel<T, D, CAUSAL, MAT>), dim3(a.nblocks), dim3(256), 0, st, a);
+}
+
+template <typename T, int D, bool CAUSAL>
+void launch_mat_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
+  a.ntiles = (a.n + kFwdBQ - 1) / kFwdBQ;
+  a.nblocks = heads * a.ntiles;
+  hipLaunchKernelGGL((attn::mat_fwd_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
 }
 
 template <typename T, int D, bool C>
@@ -101,6 +108,13 @@ struct DkvL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { laun
 template <typename T, int D, bool C>
 struct DqL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { launch_dq<T, D, C>(a, heads, st); } };
 
+template <typename T, int D, bool C>
+struct MatFwdL { static void run(attn::FwdArgs a, int heads, hipStream_t st) { launch_mat_fwd<T, D, C>(a, heads, st); } };
+template <typename T, int D, bool C>
+struct MatDkvL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { launch_dkdv<T, D, C, true>(a, heads, st); } };
+template <typename T, int D, bool C>
+struct MatDqL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { launch_dq<T, D, C, true>(a, heads, st); } };
+
 template <template <typename, int, bool> class F, typename T, typename Args>
 void by_d(int d, int causal, Args a, int heads, hipStream_t st) {
   if (d == 32) { causal ? F<T, 32, true>::run(a, heads, st) : F<T, 32, false>::run(a, heads, st); }
@@ -113,6 +127,11 @@ void run_dispatch(int dtype, int d, int causal, Args a, int heads, hipStream_t s
   if (dtype == ATTN_BF16) by_d<F, bf16>(d, causal, a, heads, st);
   else by_d<F, float>(d, causal, a, heads, st);
 }
+
+// Row stride of the materialised attention matrix: n rounded up to a
+// multiple of 128, so every key tile the kernels touch lies inside the row.
+constexpr int kMatMaxN = 1 << 20;
+long long mat_lda(int n) { return ((long long)n + 127) / 128 * 128; }
 
 }  // namespace
 
@@ -259,6 +278,132 @@ int attn_fwd_bwd_timed(const void* Q, const void* K, const void* V, const void* 
                       B, H, n, d, scale, causal, dtype, stream, events);
 }
 
+size_t attn_mat_bytes(int B, int H, int n, int dtype) {
+  if (B < 1 || H < 1 || n < 1 || n > kMatMaxN) return 0;
+  if (dtype != ATTN_BF16 && dtype != ATTN_F32) return 0;
+  const size_t e = dtype == ATTN_BF16 ? 2 : 4;
+  return (size_t)B * (size_t)H * (size_t)n * (size_t)mat_lda(n) * e;
+}
+
+static int check_mat(const void* P, size_t p_bytes, int B, int H, int n, int dtype) {
+  if (n > kMatMaxN) return ATTN_E_SHAPE;
+  if (!aligned(P, 16)) return ATTN_E_ALIGN;
+  if (p_bytes < attn_mat_bytes(B, H, n, dtype)) return ATTN_E_WORKSPACE;
+  return ATTN_OK;
+}
+
+static attn::FwdArgs mat_fwd_args(const void* Q, const void* K, const void* V, const void* dO, void* O,
+                                  float* L, void* P, float* dvec, float* lse2, int n, int d, float scale,
+                                  int dtype) {
+  const ScaleParts sp = split_scale(scale, dtype);
+  attn::FwdArgs f{};
+  f.q = Q; f.k = K; f.v = V; f.dout = dO;
+  f.o = O; f.lse = L; f.dvec = dvec; f.lse2 = lse2;
+  f.head_stride = (long long)n * d;
+  f.n = n;
+  f.sl2 = sp.sl2;
+  f.qflip = sp.qflip;
+  f.amat = P;
+  f.lda = mat_lda(n);
+  return f;
+}
+
+static attn::BwdArgs mat_bwd_args(const void* Q, const void* K, const void* V, const void* dO,
+                                  const void* P, float* dvec, void* dQ, void* dK, void* dV, int n, int d,
+                                  float scale, int dtype) {
+  const ScaleParts sp = split_scale(scale, dtype);
+  attn::BwdArgs b{};
+  b.q = Q; b.k = K; b.v = V; b.dout = dO;
+  b.lse2 = nullptr; b.dvec = dvec;
+  b.dq = dQ; b.dk = dK; b.dv = dV;
+  b.head_stride = (long long)n * d;
+  b.n = n;
+  b.sl2 = sp.sl2;
+  b.dk_scale = scale;
+  b.dq_scale = scale;
+  b.qflip = sp.qflip;
+  b.amat = P;
+  b.lda = mat_lda(n);
+  return b;
+}
+
+int attn_mat_fwd(const void* Q, const void* K, const void* V, void* O, float* L, void* P, size_t p_bytes,
+                 int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
+  if (!Q || !K || !V || !O || !L || !P) return ATTN_E_NULL;
+  int rc = check_common(B, H, n, d, scale, causal, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) || !aligned(L, 4))
+    return ATTN_E_ALIGN;
+  rc = check_mat(P, p_bytes, B, H, n, dtype);
+  if (rc != ATTN_OK) return rc;
+  const attn::FwdArgs f = mat_fwd_args(Q, K, V, nullptr, O, L, P, nullptr, nullptr, n, d, scale, dtype);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  run_dispatch<MatFwdL>(dtype, d, causal, f, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  return ATTN_OK;
+}
+
+int attn_mat_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const void* P, size_t p_bytes, void* dQ, void* dK, void* dV,
+                 void* workspace, size_t workspace_bytes,
+                 int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
+  if (!Q || !K || !V || !O || !dO || !P || !dQ || !dK || !dV || !workspace) return ATTN_E_NULL;
+  int rc = check_common(B, H, n, d, scale, causal, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16) ||
+      !aligned(dO, 16) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) ||
+      !aligned(workspace, 4))
+    return ATTN_E_ALIGN;
+  rc = check_mat(P, p_bytes, B, H, n, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (workspace_bytes < attn_workspace_bytes(B, H, n, d)) return ATTN_E_WORKSPACE;
+  float* dvec = static_cast<float*>(workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+
+  attn::PrepArgs p{};
+  p.o = O; p.dout = dO; p.lse = nullptr; p.dvec = dvec; p.lse2 = nullptr;
+  p.rows = (long long)B * H * n;
+  run_dispatch<PrepL>(dtype, d, causal, p, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  const attn::BwdArgs b = mat_bwd_args(Q, K, V, dO, P, dvec, dQ, dK, dV, n, d, scale, dtype);
+  run_dispatch<MatDkvL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  run_dispatch<MatDqL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  return ATTN_OK;
+}
+
+int attn_mat_fwd_bwd(const void* Q, const void* K, const void* V, const void* dO,
+                     void* O, float* L, void* P, size_t p_bytes, void* dQ, void* dK, void* dV,
+                     void* workspace, size_t workspace_bytes,
+                     int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
+  if (!Q || !K || !V || !dO || !O || !L || !P || !dQ || !dK || !dV || !workspace) return ATTN_E_NULL;
+  int rc = check_common(B, H, n, d, scale, causal, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(dO, 16) ||
+      !aligned(O, 16) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) ||
+      !aligned(L, 4) || !aligned(workspace, 4))
+    return ATTN_E_ALIGN;
+  rc = check_mat(P, p_bytes, B, H, n, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (workspace_bytes < attn_workspace_bytes(B, H, n, d)) return ATTN_E_WORKSPACE;
+  float* dvec = static_cast<float*>(workspace);
+  float* lse2 = dvec + (size_t)B * H * n;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  const attn::FwdArgs f = mat_fwd_args(Q, K, V, dO, O, L, P, dvec, lse2, n, d, scale, dtype);
+  run_dispatch<MatFwdL>(dtype, d, causal, f, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  const attn::BwdArgs b = mat_bwd_args(Q, K, V, dO, P, dvec, dQ, dK, dV, n, d, scale, dtype);
+  run_dispatch<MatDkvL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  run_dispatch<MatDqL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  return ATTN_OK;
+}
+
 const char* attn_strerror(int code) {
   switch (code) {
     case ATTN_OK: return "success";
@@ -266,7 +411,7 @@ const char* attn_strerror(int code) {
     case ATTN_E_SHAPE: return "B, H or n < 1, or the problem is too large to index";
     case ATTN_E_UNSUPPORTED: return "unsupported head dimension (d must be 32, 64 or 128) or dtype";
     case ATTN_E_ALIGN: return "a tensor is not 16-byte aligned (L and workspace: 4-byte)";
-    case ATTN_E_WORKSPACE: return "workspace smaller than attn_workspace_bytes()";
+    case ATTN_E_WORKSPACE: return "workspace smaller than attn_workspace_bytes(), or P smaller than attn_mat_bytes()";
     case ATTN_E_HIP: return "the HIP runtime rejected a kernel launch";
     case ATTN_E_ARG: return "scale is not finite, or causal is not 0 or 1";
     default: return "unknown attn status code";

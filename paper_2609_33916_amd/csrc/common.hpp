@@ -368,6 +368,42 @@ template <int ROWS, int D, int NW> struct TileLoader16 {
   }
 };
 
+// Global -> LDS DMA of a ROWS x COLS block of a bf16 matrix with a runtime
+// row stride `ld` (elements): the same LDS layout as TileLoader16<ROWS, COLS,
+// NW> (natural rows, swz16<COLS> chunks), so tr_read16<COLS> reads it. `g`
+// points at the block's first column in matrix row 0; rows >= n fetch row
+// n - 1.
+template <int ROWS, int COLS, int NW> struct BlockLoader16 {
+  static constexpr int C = COLS / 8;
+  static constexpr int TI = ROWS * COLS * 2 / 1024;
+  static constexpr int NI = (TI + NW - 1) / NW;
+  static_assert(ROWS * COLS * 2 == TI * 1024, "block must split into 1 KB wave blocks");
+  int off[NI];
+  int xr[NI];
+  int ld;
+  __device__ __forceinline__ BlockLoader16(int w, int lane, int ld_) : ld(ld_) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int L = 64 * (w + NW * j) + lane;
+      const int s = L / C, slot = L % C;
+      xr[j] = s;
+      off[j] = s * ld + 8 * (slot ^ swz16<COLS>(s));
+    }
+  }
+  __device__ __forceinline__ void issue(bf16* lds, const bf16* g, int row0, int n, int w) const {
+    const bool full = row0 + ROWS <= n;
+    const bf16* base = g + (size_t)row0 * ld;
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      if (TI % NW == 0 || w + NW * j < TI) {
+        int o = off[j];
+        if (!full && row0 + xr[j] >= n) o -= (row0 + xr[j] - (n - 1)) * ld;
+        __builtin_amdgcn_global_load_lds(base + o, (ATTN_LDS void*)(lds + 512 * (w + NW * j)), 16, 0, 0);
+      }
+    }
+  }
+};
+
 // Row read (16-wide): A operand = tile rows 16*rb + c, k-step t covers
 // d in [32t, 32t + 32), lane group g takes d in [32t + 8g, +8).
 template <int D>
@@ -423,6 +459,25 @@ template <> struct Quad<float> {
     *(f32x4*)p = (f32x4){a, b, c, d};
   }
   __device__ __forceinline__ static f32x4 load(const float* p) { return *(const f32x4*)p; }
+};
+
+// 16 consecutive row elements (an accumulator column j = 0..15 of one lane)
+// stored as 16-byte chunks.
+template <typename T> struct Run16;
+template <> struct Run16<bf16> {
+  __device__ __forceinline__ static void store(bf16* p, const f32x16& v) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+      *(u32x4*)(p + 8 * e) = (u32x4){pack_bf16x2(v[8 * e], v[8 * e + 1]), pack_bf16x2(v[8 * e + 2], v[8 * e + 3]),
+                                     pack_bf16x2(v[8 * e + 4], v[8 * e + 5]),
+                                     pack_bf16x2(v[8 * e + 6], v[8 * e + 7])};
+  }
+};
+template <> struct Run16<float> {
+  __device__ __forceinline__ static void store(float* p, const f32x16& v) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) *(f32x4*)(p + 4 * e) = (f32x4){v[4 * e], v[4 * e + 1], v[4 * e + 2], v[4 * e + 3]};
+  }
 };
 
 // --------------------------------------------------------- scheduling --

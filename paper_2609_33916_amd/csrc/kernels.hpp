@@ -42,6 +42,8 @@ struct FwdArgs {
   int nblocks;   // grid size
   float sl2;     // |scale| * log2(e), clamped away from 0
   uint32_t qflip;  // sign-bit mask applied to Q (negative scale)
+  void* amat;      // materialising forward only: the attention matrix P
+  long long lda;   // its row stride in elements (a multiple of 128)
 };
 
 struct BwdArgs {
@@ -62,6 +64,8 @@ struct BwdArgs {
   float dk_scale;  // scale (dK = s dS^T Q; K is read sign-flipped when scale < 0)
   float dq_scale;  // scale
   uint32_t qflip;
+  const void* amat;  // materialising backward only: the stored P, read instead of recomputed
+  long long lda;
 };
 
 // ======================================================================
@@ -107,7 +111,7 @@ __global__ void __launch_bounds__(256) bwd_prep_kernel(const PrepArgs a) {
   for (int off = G / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
   if (row < a.rows && part == 0) {
     a.dvec[row] = acc;
-    a.lse2[row] = a.lse[row] * kLog2e;
+    if (a.lse) a.lse2[row] = a.lse[row] * kLog2e;
   }
 }
 
@@ -273,14 +277,195 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
 }
 
 // ======================================================================
+// Materialising forward: the naive realisation in which the attention matrix
+// is written to memory for the backward to read (Fig. fig:concept; the A
+// array of Table tab:paper1-dram). Same tiling as fwd_kernel, two sweeps over
+// the key tiles:
+//   1. S^T = K Q^T for every tile, keeping each query's running maximum and
+//      sum of 2^(S sl2 - max): the base-2 log-sum-exp L2 of the row;
+//   2. S^T again, P = 2^(S sl2 - L2) (already normalised), P stored to row qi
+//      of the matrix (input dtype, row stride lda, zeros where masked) and
+//      O^T += V^T P^T.
+// Each wave writes every key tile it visits in full (64 keys) for its 32
+// queries; under the causal mask tiles that lie wholly after the wave's
+// last query are neither visited nor written.
+// ======================================================================
+template <typename T, int D, bool CAUSAL>
+__global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
+  using E = Elem<T>;
+  using Frag = typename E::frag;
+  constexpr int BQ = 128, BKV = 64, NKB = BKV / 32, NDB = D / 32;
+  constexpr int KP = E::KP;
+  constexpr int TD = D / (2 * KP);
+  constexpr int T32 = 16 / KP;
+  using TL = Tile<T, BKV, D>;
+  __shared__ __attribute__((aligned(16))) T stA[2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) T stB[2][TL::ELEMS];
+
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int head, qt;
+  block_map(blockIdx.x, a.nblocks, a.ntiles, CAUSAL, head, qt);
+  const int n = a.n;
+  const size_t hoff = (size_t)head * (size_t)a.head_stride;
+  const T* Qg = (const T*)a.q + hoff;
+  const T* Kg = (const T*)a.k + hoff;
+  const T* Vg = (const T*)a.v + hoff;
+  const int q0 = qt * BQ, qw0 = q0 + 32 * w, qi = qw0 + c;
+  T* Arow = (T*)a.amat + (size_t)head * n * a.lda + (size_t)qi * a.lda;
+
+  RowFrags<T, D> qf;
+  qf.load(Qg, qi, n, h, a.qflip);
+
+  const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
+  const int nt = (kv_end + BKV - 1) / BKV;
+  const float sl2 = a.sl2;
+  TileLoader<T, BKV, D> kld(w, lane), vld(w, lane);
+
+  // raw scores of key tile kv0 for this lane's query (masked to -inf)
+  auto scores = [&](const T* kl, int kv0, f32x16 (&s)[NKB]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < NKB; ++b) {
+      s[b] = zero16();
+#pragma unroll
+      for (int t = 0; t < TD; ++t) mma(s[b], RowRead<T, D>::get(kl, b, t, h, c), qf.f[t]);
+    }
+    const bool edge = (kv0 + BKV > n) || (CAUSAL && kv0 + BKV - 1 > qw0);
+    if (edge) {
+#pragma unroll
+      for (int b = 0; b < NKB; ++b)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int key = kv0 + 32 * b + 16 * h + j;
+          if (key >= n || (CAUSAL && key > qi)) s[b][j] = -INFINITY;
+        }
+    }
+  };
+
+  // ---- sweep 1: row maximum and sum, K tiles only
+  kld.issue(stA[0], Kg, 0, n, w);
+  kld.commit(stA[0]);
+  __syncthreads();
+  float m_run = -INFINITY, lsum = 0.f;
+  auto sweep1 = [&](int it, T (&cur)[2][TL::ELEMS], T (&nxt)[2][TL::ELEMS]) __attribute__((always_inline)) {
+    const int kv0 = it * BKV;
+    if (it + 1 < nt) kld.issue(nxt[0], Kg, kv0 + BKV, n, w);
+    if (!CAUSAL || kv0 <= qw0 + 31) {
+      f32x16 s[NKB];
+      scores(cur[0], kv0, s);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int b = 0; b < NKB; ++b)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[b][j]);
+      const float mt = halves_max(mx) * sl2;
+      if (mt > m_run) {
+        lsum *= exp2_fast(m_run - mt);
+        m_run = mt;
+      }
+      const float mb = (m_run == -INFINITY) ? 0.f : -m_run;
+      float rs = 0.f;
+#pragma unroll
+      for (int b = 0; b < NKB; ++b)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) rs += exp2_fast(fmaf(s[b][j], sl2, mb));
+      lsum += rs;
+    }
+    if (it + 1 < nt) kld.commit(nxt[0]);
+    __syncthreads();
+  };
+  for (int it = 0; it < nt; it += 2) {
+    sweep1(it, stA, stB);
+    if (it + 1 < nt) sweep1(it + 1, stB, stA);
+  }
+  const float ltot = halves_sum(lsum);
+  const float l2 = m_run + log2f(ltot);
+
+  // ---- sweep 2: normalised P to memory and O = P V
+  kld.issue(stA[0], Kg, 0, n, w);
+  vld.issue(stA[1], Vg, 0, n, w);
+  kld.commit(stA[0]);
+  vld.commit(stA[1]);
+  __syncthreads();
+  f32x16 oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = zero16();
+  auto sweep2 = [&](int it, T (&cur)[2][TL::ELEMS], T (&nxt)[2][TL::ELEMS]) __attribute__((always_inline)) {
+    const int kv0 = it * BKV;
+    if (it + 1 < nt) {
+      kld.issue(nxt[0], Kg, kv0 + BKV, n, w);
+      vld.issue(nxt[1], Vg, kv0 + BKV, n, w);
+    }
+    if (!CAUSAL || kv0 <= qw0 + 31) {
+      f32x16 s[NKB];
+      scores(cur[0], kv0, s);
+#pragma unroll
+      for (int b = 0; b < NKB; ++b) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) s[b][j] = exp2_fast(fmaf(s[b][j], sl2, -l2));
+        if (qi < n) Run16<T>::store(Arow + kv0 + 32 * b + 16 * h, s[b]);
+      }
+#pragma unroll
+      for (int b = 0; b < NKB; ++b)
+#pragma unroll
+        for (int t = 0; t < T32; ++t) {
+          const Frag pf = FragFromAcc<T>::get(s[b], t);
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) mma(oacc[db], TransRead<T, D>::get(cur[1], b, db, t, h, c), pf);
+        }
+    }
+    if (it + 1 < nt) {
+      kld.commit(nxt[0]);
+      vld.commit(nxt[1]);
+    }
+    __syncthreads();
+  };
+  for (int it = 0; it < nt; it += 2) {
+    sweep2(it, stA, stB);
+    if (it + 1 < nt) sweep2(it + 1, stB, stA);
+  }
+
+  // ---- epilogue: O, L and (with dO) the backward's D and base-2 L rows
+  T* Og = (T*)a.o + hoff;
+  const T* dOg = a.dout ? (const T*)a.dout + hoff : nullptr;
+  float dpart = 0.f;
+  if (qi < n) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int col = 32 * db + 8 * q4 + 4 * h;
+        const float o0 = oacc[db][4 * q4 + 0], o1 = oacc[db][4 * q4 + 1];
+        const float o2 = oacc[db][4 * q4 + 2], o3 = oacc[db][4 * q4 + 3];
+        Quad<T>::store(Og + (size_t)qi * D + col, o0, o1, o2, o3);
+        if (dOg) {
+          const f32x4 g = Quad<T>::load(dOg + (size_t)qi * D + col);
+          dpart += o0 * g[0] + o1 * g[1] + o2 * g[2] + o3 * g[3];
+        }
+      }
+  }
+  const float dsum = halves_sum(dpart);
+  if (qi < n && h == 0) {
+    const size_t row = (size_t)head * n + qi;
+    a.lse[row] = l2 * kLn2;
+    if (dOg) {
+      a.dvec[row] = dsum;
+      a.lse2[row] = l2;
+    }
+  }
+}
+
+// ======================================================================
 // dK, dV: a workgroup owns BKV = 128 keys (32 per wave, held in registers as
 // B operands); Q and dO tiles of BQ = 64 queries are staged in LDS with
 // their base-2 log-sum-exp and D rows.
 // Per wave and 32-query block:  S = Q K^T, dP = dO V^T  (rows = queries,
 // cols = the wave's keys), P = 2^(S sl2 - L), dS = P (dP - D),
 // dV^T += dO^T P, dK^T += Q^T dS.
+// With MAT (materialising backward) S is not recomputed: each lane reads its
+// column of P (16 query rows) straight from the stored matrix.
 // ======================================================================
-template <typename T, int D, bool CAUSAL>
+template <typename T, int D, bool CAUSAL, bool MAT = false>
 __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   using E = Elem<T>;
   using Frag = typename E::frag;
@@ -312,8 +497,9 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   // K is read sign-flipped for a negative scale (S = |s| Q (-K)^T), so the
   // Q tiles stay as stored and dK takes the signed scale
   RowFrags<T, D> kf, vf;
-  kf.load(Kg, kj, n, h, a.qflip);
+  if (!MAT) kf.load(Kg, kj, n, h, a.qflip);
   vf.load(Vg, kj, n, h, 0u);
+  const T* Ag = MAT ? (const T*)a.amat + (size_t)head * n * a.lda : nullptr;
 
   const int q_begin = CAUSAL ? (k0 / BQ) * BQ : 0;
   const int nt = (n - q_begin + BQ - 1) / BQ;
@@ -324,7 +510,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   auto load_rows = [&](int r0, T (&tl)[2][TL::ELEMS], float (&ld)[2][BQ]) __attribute__((always_inline)) {
     qld.issue(tl[0], Qg, r0, n, w);
     dold.issue(tl[1], dOg, r0, n, w);
-    if (w < 2) {
+    if (w < 2 && (!MAT || w == 1)) {   // MAT reads no L rows
       const int r = min(r0 + lane, n - 1);
       __builtin_amdgcn_global_load_lds((w == 0 ? Lg : Dg) + r, (ATTN_LDS void*)(ld[w]), 4, 0, 0);
     }
@@ -353,9 +539,17 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
       const int qb0 = qt0 + 32 * qb;
       if (CAUSAL && qb0 + 31 < kw0) continue;  // every query of the block precedes every key
       f32x16 s = zero16(), dp = zero16();
+      if constexpr (MAT) {
+        // lane (h, c): P of query qb0 + 16h + j, key kj (rows or keys >= n read as 0)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int q = qb0 + 16 * h + j;
+          s[j] = (q < n && kj < n) ? (float)Ag[(size_t)q * a.lda + kj] : 0.f;
+        }
+      }
 #pragma unroll
       for (int t = 0; t < D / (2 * KP); ++t) {
-        mma(s, RowRead<T, D>::get(ql, qb, t, h, c), kf.f[t]);
+        if (!MAT) mma(s, RowRead<T, D>::get(ql, qb, t, h, c), kf.f[t]);
         mma(dp, RowRead<T, D>::get(dol, qb, t, h, c), vf.f[t]);
       }
       // lane (h, c): element j is query qb0 + 16h + j, key kj
@@ -368,7 +562,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int j = 4 * j4 + e;
-          float p = exp2_fast(fmaf(s[j], sl2, -l4[e]));
+          float p = MAT ? s[j] : exp2_fast(fmaf(s[j], sl2, -l4[e]));
           if (edge) {
             const int q = qb0 + 16 * h + j;
             if (q >= n || (CAUSAL && kj > q)) p = 0.f;
@@ -424,14 +618,20 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 //   S = Q K^T, dP = dO V^T          (two 16-query blocks each)
 //   P = 2^(S sl2 - L), dS = P (dP - D)
 //   dV^T += dO^T P, dK^T += Q^T dS  (contraction over the 32 queries)
+// With MAT (the backward of the materialising path) S and the exponentials
+// are not recomputed: the BQ x 16NW block of the stored P is staged in LDS
+// next to Q and dO, and its transposed read is directly the P operand.
 // ======================================================================
-template <int D, bool CAUSAL, int NW, int BQ>
+template <int D, bool CAUSAL, int NW, int BQ, bool MAT = false>
 __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   constexpr int BKV = 16 * NW, NPB = BQ / 32, TD = D / 32, NDB = D / 16;
+  constexpr int PT = MAT ? BQ * BKV : 8;
   __shared__ __attribute__((aligned(16))) bf16 stA[2][BQ * D];
   __shared__ __attribute__((aligned(16))) bf16 stB[2][BQ * D];
   __shared__ __attribute__((aligned(16))) float ldA[2][BQ];
   __shared__ __attribute__((aligned(16))) float ldB[2][BQ];
+  __shared__ __attribute__((aligned(16))) bf16 ptA[PT];
+  __shared__ __attribute__((aligned(16))) bf16 ptB[PT];
 
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -446,15 +646,16 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   const float* Lg = a.lse2 + (size_t)head * n;
   const float* Dg = a.dvec + (size_t)head * n;
   const int k0 = kt * BKV, kw0 = k0 + 16 * w, kj = kw0 + c;
+  const bf16* Ag = MAT ? (const bf16*)a.amat + (size_t)head * n * a.lda + k0 : nullptr;
 
   // B operands: row kj of K (sign-flipped for a negative scale) and of V;
-  // k-step t holds d in [32t + 8g, +8)
+  // k-step t holds d in [32t + 8g, +8). K is only needed to recompute S.
   bf16x8 kf[TD], vf[TD];
 #pragma unroll
   for (int t = 0; t < TD; ++t) {
     u32x4 x = {0u, 0u, 0u, 0u}, y = {0u, 0u, 0u, 0u};
     if (kj < n) {
-      x = *(const u32x4*)(Kg + (size_t)kj * D + 32 * t + 8 * g);
+      if (!MAT) x = *(const u32x4*)(Kg + (size_t)kj * D + 32 * t + 8 * g);
       y = *(const u32x4*)(Vg + (size_t)kj * D + 32 * t + 8 * g);
     }
     x ^= (u32x4){a.qflip, a.qflip, a.qflip, a.qflip};
@@ -466,16 +667,19 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   const int nt = (n - q_begin + BQ - 1) / BQ;
 
   TileLoader16<BQ, D, NW> tld(w, lane);
-  auto load_rows = [&](int r0, bf16 (&tl)[2][BQ * D], float (&lr)[2][BQ]) __attribute__((always_inline)) {
+  BlockLoader16<BQ, BKV, NW> pld(w, lane, MAT ? (int)a.lda : 0);
+  auto load_rows = [&](int r0, bf16 (&tl)[2][BQ * D], float (&lr)[2][BQ], bf16 (&pt)[PT])
+      __attribute__((always_inline)) {
     tld.issue(tl[0], Qg, r0, n, w);
     tld.issue(tl[1], dOg, r0, n, w);
-    if (w < 2) {
+    if constexpr (MAT) pld.issue(pt, Ag, r0, n, w);
+    if (w < 2 && (!MAT || w == 1)) {
       const int r = min(r0 + lane, n - 1);
       if (lane < BQ)
         __builtin_amdgcn_global_load_lds((w == 0 ? Lg : Dg) + r, (ATTN_LDS void*)(lr[w]), 4, 0, 0);
     }
   };
-  load_rows(q_begin, stA, ldA);
+  load_rows(q_begin, stA, ldA, ptA);
   __syncthreads();
 
   f32x4 dk[NDB], dv[NDB];
@@ -486,7 +690,8 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   }
   const float sl2 = a.sl2;
 
-  // S and dP of pair block pb (queries 32pb + [0, 32) of the staged tile)
+  // S (unless MAT) and dP of pair block pb (queries 32pb + [0, 32) of the
+  // staged tile)
   auto sdp = [&](const bf16* ql, const bf16* dol, int pb, f32x4 (&sv)[2], f32x4 (&pv)[2])
       __attribute__((always_inline)) {
 #pragma unroll
@@ -498,30 +703,38 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
     for (int t = 0; t < TD; ++t)
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
-        mma16(sv[x], row_read16<D>(ql, 2 * pb + x, t, g, c), kf[t]);
+        if (!MAT) mma16(sv[x], row_read16<D>(ql, 2 * pb + x, t, g, c), kf[t]);
         mma16(pv[x], row_read16<D>(dol, 2 * pb + x, t, g, c), vf[t]);
       }
   };
-  // P = 2^(S sl2 - L), dS = P (dP - D) as bf16 operands; with MASK, queries
-  // >= n and (causal) queries before key kj get P = 0
-  auto softmax = [&](const float (&lr)[2][BQ], int pb, int qp0, f32x4 (&sv)[2], f32x4 (&pv)[2],
-                     bf16x8& pf, bf16x8& sf, auto mask) __attribute__((always_inline)) {
+  // P = 2^(S sl2 - L) (MAT: P from the staged block), dS = P (dP - D) as
+  // bf16 operands; with MASK, queries >= n, keys >= n and (causal) queries
+  // before key kj get P = 0
+  auto softmax = [&](const float (&lr)[2][BQ], const bf16* pt, int pb, int qp0, f32x4 (&sv)[2],
+                     f32x4 (&pv)[2], bf16x8& pf, bf16x8& sf, auto mask) __attribute__((always_inline)) {
+    constexpr bool M = decltype(mask)::value;
+    bf16x8 praw;
+    if constexpr (MAT) praw = tr_read16<BKV>(pt, 32 * pb, w, g, c);
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-      const f32x4 l4 = *(const f32x4*)&lr[0][32 * pb + 16 * x + 4 * g];
       const f32x4 d4 = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
+      f32x4 l4;
+      if constexpr (!MAT) l4 = *(const f32x4*)&lr[0][32 * pb + 16 * x + 4 * g];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        float p = exp2_fast(fmaf(sv[x][j], sl2, -l4[j]));
-        if constexpr (decltype(mask)::value) {
+        float p;
+        if constexpr (MAT) p = (float)praw[4 * x + j];
+        else p = exp2_fast(fmaf(sv[x][j], sl2, -l4[j]));
+        if constexpr (M) {
           const int q = qp0 + 16 * x + 4 * g + j;
-          if (q >= n || (CAUSAL && kj > q)) p = 0.f;
+          if (q >= n || (CAUSAL && kj > q) || (MAT && kj >= n)) p = 0.f;
         }
         sv[x][j] = p;
         pv[x][j] = p * (pv[x][j] - d4[j]);
       }
     }
-    pf = frag16(sv[0], sv[1]);
+    if constexpr (MAT && !M) pf = praw;
+    else pf = frag16(sv[0], sv[1]);
     sf = frag16(pv[0], pv[1]);
   };
   auto dvdk = [&](const bf16* ql, const bf16* dol, int pb, const bf16x8& pf, const bf16x8& sf)
@@ -533,12 +746,13 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
     }
   };
 
-  // Tiles that touch the diagonal or the end of the sequence: pair blocks
-  // one after another, with masks.
-  auto step_edge = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&nxt)[2][BQ * D],
-                       float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
+  // Pair blocks one after another; with MASK (tiles that touch the diagonal
+  // or the end of the sequence) the masks are applied.
+  auto step_seq = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT],
+                      bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], auto mask)
+      __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
-    if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt);
+    if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, pnxt);
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
       const int qp0 = qt0 + 32 * pb;
@@ -546,7 +760,7 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
       f32x4 sv[2], pv[2];
       bf16x8 pf, sf;
       sdp(cur[0], cur[1], pb, sv, pv);
-      softmax(lcur, pb, qp0, sv, pv, pf, sf, std::true_type{});
+      softmax(lcur, pcur, pb, qp0, sv, pv, pf, sf, mask);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
     __syncthreads();
@@ -555,17 +769,18 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   // valid): software-pipelined, the S/dP products of pair block pb + 1 are
   // issued next to the exponentials of pair block pb, whose dV/dK products
   // follow.
-  auto step_inner = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&nxt)[2][BQ * D],
-                        float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
+  auto step_inner = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT],
+                        bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT])
+      __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
-    if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt);
+    if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, pnxt);
     f32x4 sv[2][2], pv[2][2];
     sdp(cur[0], cur[1], 0, sv[0], pv[0]);
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
       if (pb + 1 < NPB) sdp(cur[0], cur[1], pb + 1, sv[(pb + 1) & 1], pv[(pb + 1) & 1]);
       bf16x8 pf, sf;
-      softmax(lcur, pb, qt0 + 32 * pb, sv[pb & 1], pv[pb & 1], pf, sf, std::false_type{});
+      softmax(lcur, pcur, pb, qt0 + 32 * pb, sv[pb & 1], pv[pb & 1], pf, sf, std::false_type{});
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
     // schedule: S/dP of block 0 with its row reads running ahead; then per
@@ -593,18 +808,23 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
     }
     __syncthreads();
   };
-  auto step = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&nxt)[2][BQ * D],
-                  float (&lnxt)[2][BQ]) __attribute__((always_inline)) {
+  auto step = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT],
+                  bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT]) __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
-    // the pipelined form pays off at d = 128; at smaller d a pair block has
-    // too few products to hide the exponentials behind
-    const bool inner = D == 128 && qt0 + BQ <= n && (!CAUSAL || qt0 >= k0 + BKV - 1);
-    if (inner) step_inner(it, cur, lcur, nxt, lnxt);
-    else step_edge(it, cur, lcur, nxt, lnxt);
+    const bool interior = qt0 + BQ <= n && (!CAUSAL || qt0 >= k0 + BKV - 1) && (!MAT || k0 + BKV <= n);
+    // the pipelined form pays off at d = 128 when S is recomputed; at smaller
+    // d a pair block has too few products to hide the exponentials behind
+    if constexpr (D == 128 && !MAT) {
+      if (interior) step_inner(it, cur, lcur, pcur, nxt, lnxt, pnxt);
+      else step_seq(it, cur, lcur, pcur, nxt, lnxt, pnxt, std::true_type{});
+    } else {
+      if (interior && MAT) step_seq(it, cur, lcur, pcur, nxt, lnxt, pnxt, std::false_type{});
+      else step_seq(it, cur, lcur, pcur, nxt, lnxt, pnxt, std::true_type{});
+    }
   };
   for (int it = 0; it < nt; it += 2) {
-    step(it, stA, ldA, stB, ldB);
-    if (it + 1 < nt) step(it + 1, stB, ldB, stA, ldA);
+    step(it, stA, ldA, ptA, stB, ldB, ptB);
+    if (it + 1 < nt) step(it + 1, stB, ldB, ptB, stA, ldA, ptA);
   }
 
   if (kj < n) {
@@ -627,8 +847,11 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
 // are staged in LDS.
 // Per wave and 32-key block:  S^T = K Q^T, dP^T = V dO^T (rows = keys,
 // cols = the wave's queries), dS^T = P^T (dP^T - D), dQ^T += K^T dS^T.
+// With MAT (materialising backward) S is not recomputed: the lane's 16 P
+// values of a key block are 16 consecutive elements of its query's row of
+// the stored matrix (bf16: loaded one key tile ahead into registers).
 // ======================================================================
-template <typename T, int D, bool CAUSAL>
+template <typename T, int D, bool CAUSAL, bool MAT = false>
 __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
   using E = Elem<T>;
   using Frag = typename E::frag;
@@ -653,10 +876,29 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
   const int q0 = qt * BQ, qw0 = q0 + 32 * w, qi = qw0 + c;
 
   RowFrags<T, D> qf, of;
-  qf.load(Qg, qi, n, h, a.qflip);
+  if (!MAT) qf.load(Qg, qi, n, h, a.qflip);
   of.load(dOg, qi, n, h, 0u);
-  const float lq = (qi < n) ? a.lse2[(size_t)head * n + qi] : 0.f;
+  const float lq = (!MAT && qi < n) ? a.lse2[(size_t)head * n + qi] : 0.f;
   const float dq_ = (qi < n) ? a.dvec[(size_t)head * n + qi] : 0.f;
+
+  // stored P: 16-byte chunks of this lane's row, PC chunks per 16 elements
+  constexpr int PC = sizeof(T), PCH = Elem<T>::CH;
+  constexpr bool PREF = MAT && sizeof(T) == 2;   // float32: loaded at the top of the step
+  const T* Arow = MAT ? (const T*)a.amat + (size_t)head * n * a.lda + (size_t)min(qi, n - 1) * a.lda : nullptr;
+  auto pload = [&](int kv0, u32x4 (&r)[2][PC]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < PC; ++e) r[kb][e] = *(const u32x4*)(Arow + kv0 + 32 * kb + 16 * h + PCH * e);
+  };
+  auto pget = [&](const u32x4 (&r)[PC], int j) __attribute__((always_inline)) -> float {
+    if constexpr (sizeof(T) == 2) {
+      const uint32_t x = r[j >> 3][(j & 7) >> 1];
+      return __uint_as_float((j & 1) ? (x & 0xffff0000u) : (x << 16));
+    } else {
+      return __uint_as_float(r[j >> 2][j & 3]);
+    }
+  };
 
   const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
   const int nt = (kv_end + BKV - 1) / BKV;
@@ -673,12 +915,17 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
   for (int db = 0; db < NDB; ++db) dqa[db] = zero16();
   const float sl2 = a.sl2;
 
-  auto step = [&](int it, T (&cur)[2][TL::ELEMS], T (&nxt)[2][TL::ELEMS]) __attribute__((always_inline)) {
+  u32x4 pA[2][PC], pB[2][PC];
+  if constexpr (PREF) pload(0, pA);
+  auto step = [&](int it, T (&cur)[2][TL::ELEMS], T (&nxt)[2][TL::ELEMS], u32x4 (&pc)[2][PC],
+                  u32x4 (&pn)[2][PC]) __attribute__((always_inline)) {
     const int kv0 = it * BKV;
     if (it + 1 < nt) {
       kld.issue(nxt[0], Kg, kv0 + BKV, n, w);
       vld.issue(nxt[1], Vg, kv0 + BKV, n, w);
+      if constexpr (PREF) pload(kv0 + BKV, pn);
     }
+    if constexpr (MAT && !PREF) pload(kv0, pc);
     const T* kl = cur[0];
     const T* vl = cur[1];
 #pragma unroll
@@ -688,17 +935,17 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
       f32x16 s = zero16(), dp = zero16();
 #pragma unroll
       for (int t = 0; t < D / (2 * KP); ++t) {
-        mma(s, RowRead<T, D>::get(kl, kb, t, h, c), qf.f[t]);
+        if (!MAT) mma(s, RowRead<T, D>::get(kl, kb, t, h, c), qf.f[t]);
         mma(dp, RowRead<T, D>::get(vl, kb, t, h, c), of.f[t]);
       }
       // lane (h, c): element j is key kb0 + 16h + j, query qi
-      const bool edge = (kb0 + 31 >= n) || (CAUSAL && kb0 + 31 > qw0);
+      const bool edge = (kb0 + 31 >= n) || (CAUSAL && kb0 + 31 > qw0) || (MAT && qw0 + 31 >= n);
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        float p = exp2_fast(fmaf(s[j], sl2, -lq));
+        float p = MAT ? pget(pc[kb], j) : exp2_fast(fmaf(s[j], sl2, -lq));
         if (edge) {
           const int key = kb0 + 16 * h + j;
-          if (key >= n || (CAUSAL && key > qi)) p = 0.f;
+          if (key >= n || (CAUSAL && key > qi) || (MAT && qi >= n)) p = 0.f;
         }
         dp[j] = p * (dp[j] - dq_);
       }
@@ -716,8 +963,8 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
     __syncthreads();
   };
   for (int it = 0; it < nt; it += 2) {
-    step(it, stA, stB);
-    if (it + 1 < nt) step(it + 1, stB, stA);
+    step(it, stA, stB, pA, pB);
+    if (it + 1 < nt) step(it + 1, stB, stA, pB, pA);
   }
 
   if (qi < n) {

@@ -24,6 +24,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 from typing import Dict, List
 
@@ -42,11 +43,24 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def _last_template_arg_true(kernel: str) -> bool:
+    """Whether the last template argument is `true` (demangled or mangled name)."""
+    m = re.search(r"<([^<>]*)>", kernel)
+    if m:
+        return m.group(1).split(",")[-1].strip() == "true"
+    m = re.search(r"Lb([01])EEEvNS_", kernel)
+    return bool(m and m.group(1) == "1")
+
+
 def short_name(kernel: str) -> str:
+    """Kernel name without template arguments; the backward kernels of the
+    materialising path (last template argument MAT = true) get a mat_ prefix."""
     k = kernel.replace("void ", "")
-    for key in ("fwd_kernel", "dkdv16_kernel", "dkdv_kernel", "dq_kernel", "copyBuffer",
-                "elementwise"):
+    for key in ("mat_fwd_kernel", "bwd_prep_kernel", "fwd_kernel", "dkdv16_kernel", "dkdv_kernel",
+                "dq_kernel", "copyBuffer", "elementwise"):
         if key in k:
+            if key in ("dkdv16_kernel", "dkdv_kernel", "dq_kernel") and _last_template_arg_true(k):
+                return "mat_" + key
             return key
     return k.split("(")[0][:40]
 

@@ -108,6 +108,52 @@ def test_bwd_validation(L):
     assert call(wsb=1) == -5
 
 
+def test_mat_bytes(L):
+    # [B, H, n, lda] with lda = n rounded up to 128
+    assert L.attn_mat_bytes(2, 3, 100, 0) == 2 * 3 * 100 * 128 * 2
+    assert L.attn_mat_bytes(1, 1, 128, 1) == 128 * 128 * 4
+    assert L.attn_mat_bytes(1, 1, 129, 1) == 129 * 256 * 4
+    assert L.attn_mat_bytes(128, 1, 4096, 0) == 128 * 4096 * 4096 * 2
+    assert L.attn_mat_bytes(1, 1, 0, 0) == 0
+    assert L.attn_mat_bytes(1, 1, 8, 5) == 0
+    assert L.attn_mat_bytes(1, 1, (1 << 20) + 1, 0) == 0
+
+
+def test_mat_validation(L):
+    P_OK = 1 << 40
+
+    def fwd(P=FAKE, pb=P_OK, n=8, **kw):
+        p = {k: FAKE for k in ("Q", "K", "V", "O", "L")}
+        p.update(kw)
+        return L.attn_mat_fwd(p["Q"], p["K"], p["V"], p["O"], p["L"], P, pb, 1, 1, n, 64, 0.125, 0, 0,
+                              None)
+
+    def bwd(P=FAKE, pb=P_OK, wsb=1 << 30, **kw):
+        p = {k: FAKE for k in ("Q", "K", "V", "O", "dO", "dQ", "dK", "dV", "ws")}
+        p.update(kw)
+        return L.attn_mat_bwd(p["Q"], p["K"], p["V"], p["O"], p["dO"], P, pb, p["dQ"], p["dK"],
+                              p["dV"], p["ws"], wsb, 1, 1, 8, 64, 0.125, 1, 0, None)
+
+    def fb(P=FAKE, pb=P_OK, wsb=1 << 30, **kw):
+        p = {k: FAKE for k in ("Q", "K", "V", "dO", "O", "L", "dQ", "dK", "dV", "ws")}
+        p.update(kw)
+        return L.attn_mat_fwd_bwd(p["Q"], p["K"], p["V"], p["dO"], p["O"], p["L"], P, pb, p["dQ"],
+                                  p["dK"], p["dV"], p["ws"], wsb, 1, 1, 8, 64, 0.125, 0, 1, None)
+
+    # fwd and bwd above are bfloat16 (P needs 8 * 128 * 2 bytes), fb float32
+    for call, names, need in ((fwd, ("Q", "K", "V", "O", "L"), 8 * 128 * 2),
+                              (bwd, ("Q", "K", "V", "O", "dO", "dQ", "dK", "dV", "ws"), 8 * 128 * 2),
+                              (fb, ("Q", "K", "V", "dO", "O", "L", "dQ", "dK", "dV", "ws"), 8 * 128 * 4)):
+        assert call(P=None) == -1
+        assert call(P=MIS) == -4
+        for name in names:
+            assert call(**{name: None}) == -1, (call.__name__, name)
+        assert call(pb=need - 1) == -5
+    assert bwd(wsb=1) == -5
+    assert fb(wsb=1) == -5
+    assert fwd(n=(1 << 20) + 1) == -2
+
+
 def test_binding_rejects_cpu_tensors():
     import torch
     import paper_2609_33916_amd as pkg
@@ -118,7 +164,8 @@ def test_binding_rejects_cpu_tensors():
 
 def test_library_source_never_allocates():
     """No device allocation anywhere in the library: all buffers are the
-    caller's, so nothing of size n x n can exist."""
+    caller's (the naive path's n x n P included), so the fused path can hold
+    nothing of size n x n."""
     csrc = os.path.join(ROOT, "paper_2609_33916_amd", "csrc")
     for fn in os.listdir(csrc):
         text = open(os.path.join(csrc, fn)).read()
