@@ -282,8 +282,12 @@ template <int D> struct RowRead<float, D> {
 
 // Transposed read: A operand = column 32*db + c of the tile, contraction over
 // logical rows of block rb; k-step t covers logical rows 16h + t*KP + [0, KP).
+// The bf16 tiles hold 64 rows. Offsets are reduced modulo the tile size (a
+// no-op on valid indexes): with the bound visible, the compiler can tell
+// these reads from the LDS DMA into the other stage and does not wait for it.
 template <typename T, int D> struct TransRead;
 template <int D> struct TransRead<bf16, D> {
+  static constexpr int MASK = 64 * D - 1;
   __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int db, int t, int h, int c) {
     // 16-lane group: source lane q = c % 16 reads stored row base + q/4 and
     // columns [32db + 16*(c/16) + 4*(q%4), +4); the transpose hands lane c
@@ -293,8 +297,8 @@ template <int D> struct TransRead<bf16, D> {
     const int r1 = r0 + 8;                                  // logical +4 -> stored +8
     const int ch = 4 * db + 2 * (c >> 4) + ((q & 3) >> 1);  // 16-byte chunk of the columns
     const int sub = (q & 1) * 4;
-    const bf16* p0 = s + r0 * D + ((ch ^ swz<D>(r0)) * 8) + sub;
-    const bf16* p1 = s + r1 * D + ((ch ^ swz<D>(r1)) * 8) + sub;
+    const bf16* p0 = s + ((r0 * D + ((ch ^ swz<D>(r0)) * 8) + sub) & MASK);
+    const bf16* p1 = s + ((r1 * D + ((ch ^ swz<D>(r1)) * 8) + sub) & MASK);
     i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p0));
     i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p1));
     // whole-register bit casts (element-wise 16-bit inserts are avoided)
@@ -413,15 +417,19 @@ __device__ __forceinline__ bf16x8 row_read16(const bf16* s, int rb, int t, int g
 }
 
 // Transposed read (16-wide): A operand = columns 16*db + c, k slots = rows
-// r0 + 4g + [0, 4) and r0 + 16 + 4g + [0, 4).
-template <int D>
+// r0 + 4g + [0, 4) and r0 + 16 + 4g + [0, 4) of a ROWS x D tile. Offsets are
+// reduced modulo the tile size, as in TransRead, so the compiler sees them
+// stay inside the tile.
+template <int D, int ROWS>
 __device__ __forceinline__ bf16x8 tr_read16(const bf16* s, int r0, int db, int g, int c) {
+  static_assert((ROWS * D & (ROWS * D - 1)) == 0, "tile size must be a power of two");
+  constexpr int MASK = ROWS * D - 1;
   const int ra = r0 + 4 * g + (c >> 2);
   const int rb2 = ra + 16;
   const int ch = 2 * db + ((c & 3) >> 1);
   const int sub = (c & 1) * 4;
-  const bf16* p0 = s + ra * D + 8 * (ch ^ swz16<D>(ra)) + sub;
-  const bf16* p1 = s + rb2 * D + 8 * (ch ^ swz16<D>(rb2)) + sub;
+  const bf16* p0 = s + ((ra * D + 8 * (ch ^ swz16<D>(ra)) + sub) & MASK);
+  const bf16* p1 = s + ((rb2 * D + 8 * (ch ^ swz16<D>(rb2)) + sub) & MASK);
   i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p0));
   i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p1));
   const u32x2 x = __builtin_bit_cast(u32x2, lo), y = __builtin_bit_cast(u32x2, hi);
@@ -462,23 +470,31 @@ template <> struct Quad<float> {
 };
 
 // 16 consecutive row elements (an accumulator column j = 0..15 of one lane)
-// stored as 16-byte chunks.
+// rounded to T and packed as NC 16-byte chunks (element order = memory order).
 template <typename T> struct Run16;
 template <> struct Run16<bf16> {
-  __device__ __forceinline__ static void store(bf16* p, const f32x16& v) {
+  static constexpr int NC = 2;
+  __device__ __forceinline__ static void pack(const f32x16& v, u32x4 (&r)[NC]) {
 #pragma unroll
-    for (int e = 0; e < 2; ++e)
-      *(u32x4*)(p + 8 * e) = (u32x4){pack_bf16x2(v[8 * e], v[8 * e + 1]), pack_bf16x2(v[8 * e + 2], v[8 * e + 3]),
-                                     pack_bf16x2(v[8 * e + 4], v[8 * e + 5]),
-                                     pack_bf16x2(v[8 * e + 6], v[8 * e + 7])};
+    for (int e = 0; e < NC; ++e)
+      r[e] = (u32x4){pack_bf16x2(v[8 * e], v[8 * e + 1]), pack_bf16x2(v[8 * e + 2], v[8 * e + 3]),
+                     pack_bf16x2(v[8 * e + 4], v[8 * e + 5]), pack_bf16x2(v[8 * e + 6], v[8 * e + 7])};
   }
 };
 template <> struct Run16<float> {
-  __device__ __forceinline__ static void store(float* p, const f32x16& v) {
+  static constexpr int NC = 4;
+  __device__ __forceinline__ static void pack(const f32x16& v, u32x4 (&r)[NC]) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) *(f32x4*)(p + 4 * e) = (f32x4){v[4 * e], v[4 * e + 1], v[4 * e + 2], v[4 * e + 3]};
+    for (int e = 0; e < NC; ++e)
+      r[e] = (u32x4){__float_as_uint(v[4 * e]), __float_as_uint(v[4 * e + 1]), __float_as_uint(v[4 * e + 2]),
+                     __float_as_uint(v[4 * e + 3])};
   }
 };
+template <typename T>
+__device__ __forceinline__ void store_run16(T* p, const u32x4 (&r)[Run16<T>::NC]) {
+#pragma unroll
+  for (int e = 0; e < Run16<T>::NC; ++e) *(u32x4*)(p + e * Elem<T>::CH) = r[e];
+}
 
 // --------------------------------------------------------- scheduling --
 // Workgroup id -> (head, tile). Consecutive workgroup ids are dispatched

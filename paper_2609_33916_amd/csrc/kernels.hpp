@@ -126,6 +126,7 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
   using E = Elem<T>;
   using Frag = typename E::frag;
   constexpr int BQ = 128, BKV = 64, NKB = BKV / 32, NDB = D / 32;
+  static_assert(BKV == 64, "TransRead reads 64-row tiles");
   constexpr int KP = E::KP;
   constexpr int TD = D / (2 * KP);   // k-steps over d
   constexpr int T32 = 16 / KP;       // k-steps over a 32-row block
@@ -250,6 +251,15 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
   const T* dOg = a.dout ? (const T*)a.dout + hoff : nullptr;
   float dpart = 0.f;
   if (qi < n) {
+    // all dO loads before the first O store (the two may not be proven
+    // disjoint, and a load after a store would wait for it)
+    f32x4 g[NDB][4];
+    if (dOg) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) g[db][q4] = Quad<T>::load(dOg + (size_t)qi * D + 32 * db + 8 * q4 + 4 * h);
+    }
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -258,10 +268,7 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
         const float o0 = oacc[db][4 * q4 + 0] * inv, o1 = oacc[db][4 * q4 + 1] * inv;
         const float o2 = oacc[db][4 * q4 + 2] * inv, o3 = oacc[db][4 * q4 + 3] * inv;
         Quad<T>::store(Og + (size_t)qi * D + col, o0, o1, o2, o3);
-        if (dOg) {
-          const f32x4 g = Quad<T>::load(dOg + (size_t)qi * D + col);
-          dpart += o0 * g[0] + o1 * g[1] + o2 * g[2] + o3 * g[3];
-        }
+        if (dOg) dpart += o0 * g[db][q4][0] + o1 * g[db][q4][1] + o2 * g[db][q4][2] + o3 * g[db][q4][3];
       }
   }
   const float dsum = halves_sum(dpart);
@@ -295,6 +302,7 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
   using E = Elem<T>;
   using Frag = typename E::frag;
   constexpr int BQ = 128, BKV = 64, NKB = BKV / 32, NDB = D / 32;
+  static_assert(BKV == 64, "TransRead reads 64-row tiles");
   constexpr int KP = E::KP;
   constexpr int TD = D / (2 * KP);
   constexpr int T32 = 16 / KP;
@@ -381,7 +389,9 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
   const float ltot = halves_sum(lsum);
   const float l2 = m_run + log2f(ltot);
 
-  // ---- sweep 2: normalised P to memory and O = P V
+  // ---- sweep 2: normalised P to memory and O = P V. A tile's P is kept
+  // packed in registers and written at the top of the next step, next to the
+  // next tile's LDS copies, so the waits for both overlap.
   kld.issue(stA[0], Kg, 0, n, w);
   vld.issue(stA[1], Vg, 0, n, w);
   kld.commit(stA[0]);
@@ -390,8 +400,19 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
   f32x16 oacc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) oacc[db] = zero16();
+  constexpr int NC = Run16<T>::NC;
+  u32x4 pk[NKB][NC];
+  int pk_col = -1;   // first key of the pending tile (wave-uniform), -1 if none
+  auto flush = [&]() __attribute__((always_inline)) {
+    if (pk_col >= 0 && qi < n) {
+#pragma unroll
+      for (int b = 0; b < NKB; ++b) store_run16<T>(Arow + pk_col + 32 * b + 16 * h, pk[b]);
+    }
+    pk_col = -1;
+  };
   auto sweep2 = [&](int it, T (&cur)[2][TL::ELEMS], T (&nxt)[2][TL::ELEMS]) __attribute__((always_inline)) {
     const int kv0 = it * BKV;
+    flush();
     if (it + 1 < nt) {
       kld.issue(nxt[0], Kg, kv0 + BKV, n, w);
       vld.issue(nxt[1], Vg, kv0 + BKV, n, w);
@@ -403,13 +424,16 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
       for (int b = 0; b < NKB; ++b) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) s[b][j] = exp2_fast(fmaf(s[b][j], sl2, -l2));
-        if (qi < n) Run16<T>::store(Arow + kv0 + 32 * b + 16 * h, s[b]);
+        Run16<T>::pack(s[b], pk[b]);
       }
+      pk_col = kv0;
 #pragma unroll
       for (int b = 0; b < NKB; ++b)
 #pragma unroll
         for (int t = 0; t < T32; ++t) {
-          const Frag pf = FragFromAcc<T>::get(s[b], t);
+          Frag pf;
+          if constexpr (sizeof(T) == 2) pf = __builtin_bit_cast(Frag, pk[b][t]);   // the stored values
+          else pf = FragFromAcc<T>::get(s[b], t);
 #pragma unroll
           for (int db = 0; db < NDB; ++db) mma(oacc[db], TransRead<T, D>::get(cur[1], b, db, t, h, c), pf);
         }
@@ -424,12 +448,20 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
     sweep2(it, stA, stB);
     if (it + 1 < nt) sweep2(it + 1, stB, stA);
   }
+  flush();
 
   // ---- epilogue: O, L and (with dO) the backward's D and base-2 L rows
   T* Og = (T*)a.o + hoff;
   const T* dOg = a.dout ? (const T*)a.dout + hoff : nullptr;
   float dpart = 0.f;
   if (qi < n) {
+    f32x4 g[NDB][4];   // dO loads first, as in fwd_kernel
+    if (dOg) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) g[db][q4] = Quad<T>::load(dOg + (size_t)qi * D + 32 * db + 8 * q4 + 4 * h);
+    }
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -438,10 +470,7 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
         const float o0 = oacc[db][4 * q4 + 0], o1 = oacc[db][4 * q4 + 1];
         const float o2 = oacc[db][4 * q4 + 2], o3 = oacc[db][4 * q4 + 3];
         Quad<T>::store(Og + (size_t)qi * D + col, o0, o1, o2, o3);
-        if (dOg) {
-          const f32x4 g = Quad<T>::load(dOg + (size_t)qi * D + col);
-          dpart += o0 * g[0] + o1 * g[1] + o2 * g[2] + o3 * g[3];
-        }
+        if (dOg) dpart += o0 * g[db][q4][0] + o1 * g[db][q4][1] + o2 * g[db][q4][2] + o3 * g[db][q4][3];
       }
   }
   const float dsum = halves_sum(dpart);
@@ -470,6 +499,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
   using E = Elem<T>;
   using Frag = typename E::frag;
   constexpr int BKV = 128, BQ = 64, NQB = BQ / 32, NDB = D / 32;
+  static_assert(BQ == 64, "TransRead reads 64-row tiles");
   constexpr int KP = E::KP;
   constexpr int T32 = 16 / KP;
   using TL = Tile<T, BQ, D>;
@@ -714,7 +744,7 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
                      f32x4 (&pv)[2], bf16x8& pf, bf16x8& sf, auto mask) __attribute__((always_inline)) {
     constexpr bool M = decltype(mask)::value;
     bf16x8 praw;
-    if constexpr (MAT) praw = tr_read16<BKV>(pt, 32 * pb, w, g, c);
+    if constexpr (MAT) praw = tr_read16<BKV, BQ>(pt, 32 * pb, w, g, c);
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
       const f32x4 d4 = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
@@ -741,8 +771,8 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
       __attribute__((always_inline)) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      mma16(dv[db], tr_read16<D>(dol, 32 * pb, db, g, c), pf);
-      mma16(dk[db], tr_read16<D>(ql, 32 * pb, db, g, c), sf);
+      mma16(dv[db], tr_read16<D, BQ>(dol, 32 * pb, db, g, c), pf);
+      mma16(dk[db], tr_read16<D, BQ>(ql, 32 * pb, db, g, c), sf);
     }
   };
 
@@ -856,6 +886,7 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
   using E = Elem<T>;
   using Frag = typename E::frag;
   constexpr int BQ = 128, BKV = 64, NKB = BKV / 32, NDB = D / 32;
+  static_assert(BKV == 64, "TransRead reads 64-row tiles");
   constexpr int KP = E::KP;
   constexpr int T32 = 16 / KP;
   using TL = Tile<T, BKV, D>;
