@@ -3,6 +3,7 @@
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
     python bench.py --mode fwd|bwd      attn_fwd or attn_bwd alone
     python bench.py --mode naive        fused versus the naive materialising path
+    python bench.py --mode atomic       attn_fwd_bwd versus the atomic-dQ variant
 
 One step is one attn_fwd_bwd call (forward, dK/dV and dQ kernels) over the
 whole workload, inputs resident in HBM before timing starts. Prints ONE JSON
@@ -248,6 +249,49 @@ def bench_naive(args, w, inp, dev, out, ws, hip, torch, attn) -> int:
     return 0
 
 
+def atomic_adds(B: int, H: int, n: int, d: int, causal: bool) -> int:
+    """float32 atomic adds of attn_fwd_bwd_atomic: every 128-key workgroup adds
+    d values for each query row < n of the tiles it sweeps (from its first
+    key's 64-query tile under the causal mask, from 0 otherwise)."""
+    rows = sum(n - ((k0 // 64) * 64 if causal else 0) for k0 in range(0, n, 128))
+    return B * H * d * rows
+
+
+def bench_atomic(args, w, inp, dev, out, ws, hip, torch, attn) -> int:
+    """The paper's atomic-versus-recompute trade-off on this GPU: attn_fwd_bwd
+    (dQ by a separate kernel that recomputes S and dP) against
+    attn_fwd_bwd_atomic (dQ accumulated with float32 atomics in the dK/dV
+    kernel)."""
+    q, k, v, do = dev["q"], dev["k"], dev["v"], dev["do"]
+    B, H, n, d = q.shape
+    wsa = torch.empty(attn.attn_workspace_bytes_atomic(B, H, n, d), dtype=torch.uint8, device=q.device)
+    out2 = tuple(torch.empty_like(t) for t in out)
+    fused = lambda: attn.attn_fwd_bwd(q, k, v, do, scale=w.scale, causal=w.causal, out=out, workspace=ws)
+    atom = lambda: attn.attn_fwd_bwd_atomic(q, k, v, do, scale=w.scale, causal=w.causal, out=out2,
+                                            workspace=wsa)
+    print("[bench] atomic: fused, atomic-dQ", file=sys.stderr, flush=True)
+    tf = _time_calls(fused, args.steps, args.warmup, hip, torch)
+    ta = _time_calls(atom, args.steps, args.warmup, hip, torch)
+    f_alg = workloads.alg_flops(B, H, n, d, w.causal)
+    rec = {
+        "metric": "attention fwd+bwd TFLOP/s, atomic-dQ variant (1 GPU)",
+        "value": round(f_alg / (ta[1] * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "higher_is_better": True,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "H": H, "n": n, "d": d, "causal": w.causal},
+        "atomic_ms": round(ta[0], 4), "fused_ms": round(tf[0], 4),
+        "atomic_tflops": round(f_alg / (ta[0] * 1e-3) / 1e12, 2),
+        "fused_tflops": round(f_alg / (tf[0] * 1e-3) / 1e12, 2),
+        "atomic_over_fused_time": round(ta[0] / tf[0], 4),
+        "predicted_atomic_adds": atomic_adds(B, H, n, d, w.causal),
+    }
+    torch.cuda.synchronize()
+    diff = {name: float((a.float() - b.float()).abs().max() / b.float().abs().max())
+            for name, a, b in zip(("O", "L", "dQ", "dK", "dV"), out2, out)}
+    rec["max_rel_diff_vs_fused"] = {key: float(f"{val:.3e}") for key, val in diff.items()}
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
 def measured_traffic_kernel(workload: str, kernel: str, prefix: str = "hbm_traffic"):
     """fetch/write bytes per launch of `kernel` from a committed summary, or None."""
     from paper_2609_33916_amd import profiling
@@ -263,7 +307,7 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(workloads.WORKLOADS))
-    ap.add_argument("--mode", default="fwd_bwd", choices=("fwd_bwd", "fwd", "bwd", "naive"),
+    ap.add_argument("--mode", default="fwd_bwd", choices=("fwd_bwd", "fwd", "bwd", "naive", "atomic"),
                     help="entry point timed: attn_fwd_bwd (default), attn_fwd, attn_bwd, or the "
                          "fused path against the naive materialising path")
     ap.add_argument("--no-cpu-baseline", action="store_true",
@@ -309,6 +353,8 @@ def main(argv=None) -> int:
     hip = HipEvents()
     if args.mode == "naive":
         return bench_naive(args, w, inp, dev, out, ws, hip, torch, attn)
+    if args.mode == "atomic":
+        return bench_atomic(args, w, inp, dev, out, ws, hip, torch, attn)
     if args.mode != "fwd_bwd":
         return bench_entry(args, w, inp, dev, out, ws, hip, torch, attn)
     evs = [[hip.create() for _ in range(4)] for _ in range(args.steps)]

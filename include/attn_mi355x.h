@@ -116,6 +116,31 @@ int attn_fwd_bwd_timed(const void* Q, const void* K, const void* V, const void* 
                        int B, int H, int n, int d, float scale, int causal, int dtype,
                        void* stream, void* const* events);
 
+/* ---- Atomic-dQ variant -------------------------------------------------
+ * The alternative Paper II weighs against recomputation (sections
+ * sec:paper2-atomics, sec:paper2-gk-fix): instead of a separate dQ kernel
+ * that recomputes S and dP per query block, the dK/dV kernel also forms
+ * dQ = dS K for its 128-key block and adds it to a float32 accumulator in
+ * the workspace with atomic adds, B*H*n*d*ceil(n/128) of them without a mask
+ * (about half that under the causal mask); a last pass writes
+ * dQ = scale * accumulator in bfloat16. Same results as attn_fwd_bwd within
+ * rounding; dQ's summation order depends on scheduling, so repeated calls
+ * may differ in the last bits of dQ. bfloat16 only (ATTN_E_UNSUPPORTED for
+ * float32). */
+
+/* Workspace for attn_fwd_bwd_atomic: the float32 accumulator B*H*n*d*4
+ * bytes, then the D and base-2 L rows (attn_workspace_bytes). The workspace
+ * must be 16-byte aligned. 0 for invalid sizes. */
+size_t attn_workspace_bytes_atomic(int B, int H, int n, int d);
+
+/* Forward + backward with atomic dQ: zero the accumulator, forward, one
+ * dK/dV/dQ kernel, finalize. Arguments as attn_fwd_bwd. */
+int attn_fwd_bwd_atomic(const void* Q, const void* K, const void* V, const void* dO,
+                        void* O, float* L, void* dQ, void* dK, void* dV,
+                        void* workspace, size_t workspace_bytes,
+                        int B, int H, int n, int d, float scale, int causal, int dtype,
+                        void* stream);
+
 /* ---- Naive (materialising) path --------------------------------------
  * The realisation the paper compares the fused one against: the forward
  * stores the attention matrix A = P (Table tab:paper1-dram counts it as the

@@ -26,6 +26,7 @@ import torch  # loads the process's HIP runtime before the library
 
 __all__ = ["attn_fwd", "attn_fwd_bwd", "attn_fwd_bwd_timed", "attn_bwd", "attn_workspace_bytes", "attn_strerror",
            "attn_mat_bytes", "attn_mat_lda", "attn_mat_fwd", "attn_mat_bwd", "attn_mat_fwd_bwd",
+           "attn_fwd_bwd_atomic", "attn_workspace_bytes_atomic",
            "AttnError", "lib", "LIB_PATH", "ATTN_BF16", "ATTN_F32"]
 
 # ATTN_MI355X_LIB may name another build of the same library (A/B comparison
@@ -65,6 +66,11 @@ def lib() -> ctypes.CDLL:
     L.attn_fwd_bwd_timed.restype = i
     L.attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, f, i, i, vp]
     L.attn_bwd.restype = i
+    L.attn_workspace_bytes_atomic.argtypes = [i, i, i, i]
+    L.attn_workspace_bytes_atomic.restype = sz
+    L.attn_fwd_bwd_atomic.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                      i, i, i, i, f, i, i, vp]
+    L.attn_fwd_bwd_atomic.restype = i
     L.attn_mat_bytes.argtypes = [i, i, i, i]
     L.attn_mat_bytes.restype = sz
     L.attn_mat_fwd.argtypes = [vp, vp, vp, vp, vp, vp, sz, i, i, i, i, f, i, i, vp]
@@ -302,3 +308,36 @@ def attn_mat_fwd_bwd(q, k, v, do, scale: Optional[float] = None, causal: bool = 
     if rc != 0:
         raise AttnError(rc, "attn_mat_fwd_bwd")
     return O, L, dQ, dK, dV, P
+
+
+# ------------------------------------------------------------ atomic dQ --
+def attn_workspace_bytes_atomic(B: int, H: int, n: int, d: int) -> int:
+    return int(lib().attn_workspace_bytes_atomic(B, H, n, d))
+
+
+def attn_fwd_bwd_atomic(q, k, v, do, scale: Optional[float] = None, causal: bool = False,
+                        out=None, workspace=None):
+    """Forward+backward with dQ accumulated by atomic adds in the dK/dV
+    kernel (bfloat16 only): returns (O, L, dQ, dK, dV)."""
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, n, d]")
+    for name, t in (("q", q), ("k", k), ("v", v), ("do", do)):
+        _check(name, t, q)
+    B, H, n, d = q.shape
+    if out is None:
+        O = torch.empty_like(q)
+        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
+        dQ, dK, dV = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    else:
+        O, L, dQ, dK, dV = out
+    if workspace is None:
+        workspace = torch.empty(max(attn_workspace_bytes_atomic(B, H, n, d), 16), dtype=torch.uint8,
+                                device=q.device)
+    rc = lib().attn_fwd_bwd_atomic(q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
+                                   O.data_ptr(), L.data_ptr(), dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
+                                   workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                   B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
+                                   _stream(q.device))
+    if rc != 0:
+        raise AttnError(rc, "attn_fwd_bwd_atomic")
+    return O, L, dQ, dK, dV

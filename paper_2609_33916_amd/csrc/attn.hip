@@ -86,6 +86,18 @@ void launch_dq(attn::BwdArgs a, int heads, hipStream_t st) {
   hipLaunchKernelGGL((attn::dq_kernel<T, D, CAUSAL, MAT>), dim3(a.nblocks), dim3(256), 0, st, a);
 }
 
+// atomic-dQ backward (bfloat16): the dK/dV kernel also accumulates dQ
+template <typename T, int D, bool CAUSAL>
+void launch_dkdv_aq(attn::BwdArgs a, int heads, hipStream_t st) {
+  if constexpr (std::is_same<T, bf16>::value) {
+    constexpr int bkv = 16 * kDkv16Waves;
+    a.ntiles = (a.n + bkv - 1) / bkv;
+    a.nblocks = heads * a.ntiles;
+    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, kDkv16Waves, kDkv16BQ, false, true>), dim3(a.nblocks),
+                       dim3(64 * kDkv16Waves), 0, st, a);
+  }
+}
+
 template <typename T, int D, bool CAUSAL>
 void launch_mat_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
   a.ntiles = (a.n + kFwdBQ - 1) / kFwdBQ;
@@ -114,6 +126,9 @@ template <typename T, int D, bool C>
 struct MatDkvL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { launch_dkdv<T, D, C, true>(a, heads, st); } };
 template <typename T, int D, bool C>
 struct MatDqL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { launch_dq<T, D, C, true>(a, heads, st); } };
+
+template <typename T, int D, bool C>
+struct DkvAqL { static void run(attn::BwdArgs a, int heads, hipStream_t st) { launch_dkdv_aq<T, D, C>(a, heads, st); } };
 
 template <template <typename, int, bool> class F, typename T, typename Args>
 void by_d(int d, int causal, Args a, int heads, hipStream_t st) {
@@ -400,6 +415,67 @@ int attn_mat_fwd_bwd(const void* Q, const void* K, const void* V, const void* dO
   run_dispatch<MatDkvL>(dtype, d, causal, b, B * H, st);
   if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
   run_dispatch<MatDqL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  return ATTN_OK;
+}
+
+size_t attn_workspace_bytes_atomic(int B, int H, int n, int d) {
+  if (B < 1 || H < 1 || n < 1 || (d != 32 && d != 64 && d != 128)) return 0;
+  return attn_workspace_bytes(B, H, n, d) + (size_t)B * (size_t)H * (size_t)n * (size_t)d * sizeof(float);
+}
+
+int attn_fwd_bwd_atomic(const void* Q, const void* K, const void* V, const void* dO,
+                        void* O, float* L, void* dQ, void* dK, void* dV,
+                        void* workspace, size_t workspace_bytes,
+                        int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
+  if (!Q || !K || !V || !dO || !O || !L || !dQ || !dK || !dV || !workspace) return ATTN_E_NULL;
+  int rc = check_common(B, H, n, d, scale, causal, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (dtype != ATTN_BF16) return ATTN_E_UNSUPPORTED;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(dO, 16) ||
+      !aligned(O, 16) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) ||
+      !aligned(L, 4) || !aligned(workspace, 16))
+    return ATTN_E_ALIGN;
+  if (workspace_bytes < attn_workspace_bytes_atomic(B, H, n, d)) return ATTN_E_WORKSPACE;
+  const ScaleParts sp = split_scale(scale, dtype);
+  const size_t rows = (size_t)B * H * n;
+  // accumulator first: 16-byte aligned for the vector fill and finalize
+  float* dqacc = static_cast<float*>(workspace);
+  float* dvec = dqacc + rows * d;
+  float* lse2 = dvec + rows;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+
+  const long long n8 = (long long)(rows * d / 8);
+  hipLaunchKernelGGL(attn::zero_f32_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, st, dqacc, n8);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+
+  attn::FwdArgs f{};
+  f.q = Q; f.k = K; f.v = V; f.dout = dO;
+  f.o = O; f.lse = L; f.dvec = dvec; f.lse2 = lse2;
+  f.head_stride = (long long)n * d;
+  f.n = n;
+  f.sl2 = sp.sl2;
+  f.qflip = sp.qflip;
+  run_dispatch<FwdL>(dtype, d, causal, f, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+
+  attn::BwdArgs b{};
+  b.q = Q; b.k = K; b.v = V; b.dout = dO;
+  b.lse2 = lse2; b.dvec = dvec;
+  b.dq = dQ; b.dk = dK; b.dv = dV;
+  b.head_stride = (long long)n * d;
+  b.n = n;
+  b.sl2 = sp.sl2;
+  b.dk_scale = scale;
+  b.dq_scale = scale;
+  b.qflip = sp.qflip;
+  b.dqacc = dqacc;
+  run_dispatch<DkvAqL>(dtype, d, causal, b, B * H, st);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+
+  hipLaunchKernelGGL((attn::dq_finalize_kernel<bf16>), dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, st,
+                     dqacc, static_cast<bf16*>(dQ), n8, scale);
   if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
   return ATTN_OK;
 }

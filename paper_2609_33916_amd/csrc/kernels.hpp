@@ -66,6 +66,7 @@ struct BwdArgs {
   uint32_t qflip;
   const void* amat;  // materialising backward only: the stored P, read instead of recomputed
   long long lda;
+  float* dqacc;      // atomic-dQ backward only: float32 [heads, n, d] accumulator (zeroed)
 };
 
 // ======================================================================
@@ -651,17 +652,29 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 // With MAT (the backward of the materialising path) S and the exponentials
 // are not recomputed: the BQ x 16NW block of the stored P is staged in LDS
 // next to Q and dO, and its transposed read is directly the P operand.
+// With AQ (atomic dQ, the alternative to a separate dQ pass that recomputes
+// S and dP) the workgroup also forms dQ = dS K for its keys: every wave writes
+// its dS^T rows to an LDS tile [keys][queries] (double-buffered), and one
+// step later each wave multiplies the whole tile by the workgroup's K block
+// (kept in LDS) for a 16-column slice of d and adds the result to a float32
+// accumulator in HBM with atomic adds (one per element and key block).
 // ======================================================================
-template <int D, bool CAUSAL, int NW, int BQ, bool MAT = false>
+template <int D, bool CAUSAL, int NW, int BQ, bool MAT = false, bool AQ = false>
 __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   constexpr int BKV = 16 * NW, NPB = BQ / 32, TD = D / 32, NDB = D / 16;
+  static_assert(!(MAT && AQ), "the materialising backward has its own dQ pass");
   constexpr int PT = MAT ? BQ * BKV : 8;
+  constexpr int DST = AQ ? BKV * BQ : 8;   // dS^T tile [BKV keys][BQ queries]
+  constexpr int KBL = AQ ? BKV * D : 8;    // the workgroup's K block [BKV][D]
   __shared__ __attribute__((aligned(16))) bf16 stA[2][BQ * D];
   __shared__ __attribute__((aligned(16))) bf16 stB[2][BQ * D];
   __shared__ __attribute__((aligned(16))) float ldA[2][BQ];
   __shared__ __attribute__((aligned(16))) float ldB[2][BQ];
   __shared__ __attribute__((aligned(16))) bf16 ptA[PT];
   __shared__ __attribute__((aligned(16))) bf16 ptB[PT];
+  __shared__ __attribute__((aligned(16))) bf16 dsA[DST];
+  __shared__ __attribute__((aligned(16))) bf16 dsB[DST];
+  __shared__ __attribute__((aligned(16))) bf16 kbl[KBL];
 
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -710,6 +723,10 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
     }
   };
   load_rows(q_begin, stA, ldA, ptA);
+  if constexpr (AQ) {
+    TileLoader16<BKV, D, NW> kbld(w, lane);
+    kbld.issue(kbl, Kg, k0, n, w);
+  }
   __syncthreads();
 
   f32x4 dk[NDB], dv[NDB];
@@ -757,7 +774,7 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
         else p = exp2_fast(fmaf(sv[x][j], sl2, -l4[j]));
         if constexpr (M) {
           const int q = qp0 + 16 * x + 4 * g + j;
-          if (q >= n || (CAUSAL && kj > q) || (MAT && kj >= n)) p = 0.f;
+          if (q >= n || (CAUSAL && kj > q) || ((MAT || AQ) && kj >= n)) p = 0.f;
         }
         sv[x][j] = p;
         pv[x][j] = p * (pv[x][j] - d4[j]);
@@ -766,6 +783,46 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
     if constexpr (MAT && !M) pf = praw;
     else pf = frag16(sv[0], sv[1]);
     sf = frag16(pv[0], pv[1]);
+  };
+  // AQ: the wave's dS^T rows (keys kw0 + c) of pair block pb into the
+  // [keys][queries] tile, 4 queries (8 bytes) per write
+  auto put_ds = [&](bf16* dsT, int pb, const bf16x8& sf) __attribute__((always_inline)) {
+    const int row = 16 * w + c;
+    const u32x4 x = __builtin_bit_cast(u32x4, sf);
+#pragma unroll
+    for (int hx = 0; hx < 2; ++hx) {
+      const int col = 32 * pb + 16 * hx + 4 * g;
+      *(u32x2*)(dsT + row * BQ + 8 * ((col >> 3) ^ swz16<BQ>(row)) + (col & 7)) = (u32x2){x[2 * hx], x[2 * hx + 1]};
+    }
+  };
+  // AQ: dQ of the queries of a finished step (dS^T in dsT) for this wave's
+  // output tiles: d block w % (D/16), query blocks split between the waves
+  // that share it; one float32 atomic add per element
+  float* dQacc = AQ ? a.dqacc + (size_t)head * n * D : nullptr;
+  auto dq_products = [&](const bf16* dsT, int qt0p) __attribute__((always_inline)) {
+    constexpr int NDT = D / 16, NQT = BQ / 16;
+    constexpr int WPD = NW / NDT, QPW = NQT / WPD;
+    static_assert(NW % NDT == 0 && NQT % WPD == 0, "dQ tiles must split evenly over the waves");
+    const int dblk = w % NDT, qbase = (w / NDT) * QPW;
+    // lane indexes made opaque here so that nothing of this phase is hoisted
+    // out of the loop into registers that stay live across the other phases
+    int gg = g, cc = c;
+    asm volatile("" : "+v"(gg), "+v"(cc));
+    bf16x8 kfr[BKV / 32];
+#pragma unroll
+    for (int kb = 0; kb < BKV / 32; ++kb) kfr[kb] = tr_read16<D, BKV>(kbl, 32 * kb, dblk, gg, cc);
+    // rows qt0p + 16 (qbase + i) + 4 gg + j of column 16 dblk + cc
+    float* base = dQacc + (size_t)(qt0p + 16 * qbase + 4 * gg) * D + 16 * dblk + cc;
+    const int qrow = qt0p + 16 * qbase + 4 * gg;
+#pragma unroll
+    for (int i = 0; i < QPW; ++i) {
+      f32x4 acc = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < BKV / 32; ++kb) mma16(acc, tr_read16<BQ, BKV>(dsT, 32 * kb, qbase + i, gg, cc), kfr[kb]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (qrow + 16 * i + j < n) unsafeAtomicAdd(base + (16 * i + j) * D, acc[j]);
+    }
   };
   auto dvdk = [&](const bf16* ql, const bf16* dol, int pb, const bf16x8& pf, const bf16x8& sf)
       __attribute__((always_inline)) {
@@ -776,21 +833,37 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
     }
   };
 
+  // AQ: dQ of the previous step, in a scheduling region of its own at the
+  // top of a step (its dS^T tile was completed before the last barrier)
+  auto dq_prev = [&](int it, const bf16* dprev) __attribute__((always_inline)) {
+    if constexpr (AQ) {
+      if (it > 0) {
+        __builtin_amdgcn_sched_barrier(0);
+        dq_products(dprev, q_begin + (it - 1) * BQ);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
   // Pair blocks one after another; with MASK (tiles that touch the diagonal
   // or the end of the sequence) the masks are applied.
-  auto step_seq = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT],
-                      bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], auto mask)
+  auto step_seq = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
+                      bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST], auto mask)
       __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, pnxt);
+    dq_prev(it, dprev);
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
       const int qp0 = qt0 + 32 * pb;
-      if (CAUSAL && qp0 + 31 < kw0) continue;  // every query of the block precedes every key
+      if (CAUSAL && qp0 + 31 < kw0) {  // every query of the block precedes every key
+        if constexpr (AQ) put_ds(dcur, pb, __builtin_bit_cast(bf16x8, (u32x4){0u, 0u, 0u, 0u}));
+        continue;
+      }
       f32x4 sv[2], pv[2];
       bf16x8 pf, sf;
       sdp(cur[0], cur[1], pb, sv, pv);
       softmax(lcur, pcur, pb, qp0, sv, pv, pf, sf, mask);
+      if constexpr (AQ) put_ds(dcur, pb, sf);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
     __syncthreads();
@@ -799,11 +872,12 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   // valid): software-pipelined, the S/dP products of pair block pb + 1 are
   // issued next to the exponentials of pair block pb, whose dV/dK products
   // follow.
-  auto step_inner = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT],
-                        bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT])
+  auto step_inner = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
+                        bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST])
       __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, pnxt);
+    dq_prev(it, dprev);
     f32x4 sv[2][2], pv[2][2];
     sdp(cur[0], cur[1], 0, sv[0], pv[0]);
 #pragma unroll
@@ -811,6 +885,7 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
       if (pb + 1 < NPB) sdp(cur[0], cur[1], pb + 1, sv[(pb + 1) & 1], pv[(pb + 1) & 1]);
       bf16x8 pf, sf;
       softmax(lcur, pcur, pb, qt0 + 32 * pb, sv[pb & 1], pv[pb & 1], pf, sf, std::false_type{});
+      if constexpr (AQ) put_ds(dcur, pb, sf);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
     // schedule: S/dP of block 0 with its row reads running ahead; then per
@@ -838,24 +913,27 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
     }
     __syncthreads();
   };
-  auto step = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT],
-                  bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT]) __attribute__((always_inline)) {
+  auto step = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
+                  bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST])
+      __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
-    const bool interior = qt0 + BQ <= n && (!CAUSAL || qt0 >= k0 + BKV - 1) && (!MAT || k0 + BKV <= n);
+    const bool interior = qt0 + BQ <= n && (!CAUSAL || qt0 >= k0 + BKV - 1) &&
+                          (!(MAT || AQ) || k0 + BKV <= n);
     // the pipelined form pays off at d = 128 when S is recomputed; at smaller
     // d a pair block has too few products to hide the exponentials behind
     if constexpr (D == 128 && !MAT) {
-      if (interior) step_inner(it, cur, lcur, pcur, nxt, lnxt, pnxt);
-      else step_seq(it, cur, lcur, pcur, nxt, lnxt, pnxt, std::true_type{});
+      if (interior) step_inner(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev);
+      else step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::true_type{});
     } else {
-      if (interior && MAT) step_seq(it, cur, lcur, pcur, nxt, lnxt, pnxt, std::false_type{});
-      else step_seq(it, cur, lcur, pcur, nxt, lnxt, pnxt, std::true_type{});
+      if (interior && MAT) step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::false_type{});
+      else step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::true_type{});
     }
   };
   for (int it = 0; it < nt; it += 2) {
-    step(it, stA, ldA, ptA, stB, ldB, ptB);
-    if (it + 1 < nt) step(it + 1, stB, ldB, ptB, stA, ldA, ptA);
+    step(it, stA, ldA, ptA, dsA, stB, ldB, ptB, dsB);
+    if (it + 1 < nt) step(it + 1, stB, ldB, ptB, dsB, stA, ldA, ptA, dsA);
   }
+  if constexpr (AQ) dq_products((nt - 1) & 1 ? dsB : dsA, q_begin + (nt - 1) * BQ);
 
   if (kj < n) {
     bf16* dKg = (bf16*)a.dk + hoff;
@@ -1009,6 +1087,28 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
         Quad<T>::store(dQg + (size_t)qi * D + col, dqa[db][4 * q4] * sc, dqa[db][4 * q4 + 1] * sc,
                        dqa[db][4 * q4 + 2] * sc, dqa[db][4 * q4 + 3] * sc);
       }
+  }
+}
+
+// ======================================================================
+// Atomic-dQ support: zero the float32 accumulator, then dQ = scale * acc in
+// the output dtype. HBM-bound, 8 elements per thread.
+// ======================================================================
+__global__ void __launch_bounds__(256) zero_f32_kernel(float* p, long long n8) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n8) {
+    ((f32x4*)p)[2 * i] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    ((f32x4*)p)[2 * i + 1] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) dq_finalize_kernel(const float* acc, T* dq, long long n8, float scale) {
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n8) {
+    const f32x4 x = ((const f32x4*)acc)[2 * i], y = ((const f32x4*)acc)[2 * i + 1];
+    Quad<T>::store(dq + 8 * i, x[0] * scale, x[1] * scale, x[2] * scale, x[3] * scale);
+    Quad<T>::store(dq + 8 * i + 4, y[0] * scale, y[1] * scale, y[2] * scale, y[3] * scale);
   }
 }
 

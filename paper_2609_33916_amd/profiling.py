@@ -43,6 +43,15 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def _template_args(kernel: str):
+    """Template arguments of a demangled name ("true"/"false" for the bool
+    parameters of a mangled one)."""
+    m = re.search(r"<([^<>]*)>", kernel)
+    if m:
+        return [x.strip() for x in m.group(1).split(",")]
+    return ["true" if b == "1" else "false" for b in re.findall(r"Lb([01])E", kernel)]
+
+
 def _last_template_arg_true(kernel: str) -> bool:
     """Whether the last template argument is `true` (demangled or mangled name)."""
     m = re.search(r"<([^<>]*)>", kernel)
@@ -56,9 +65,11 @@ def short_name(kernel: str) -> str:
     """Kernel name without template arguments; the backward kernels of the
     materialising path (last template argument MAT = true) get a mat_ prefix."""
     k = kernel.replace("void ", "")
-    for key in ("mat_fwd_kernel", "bwd_prep_kernel", "fwd_kernel", "dkdv16_kernel", "dkdv_kernel",
-                "dq_kernel", "copyBuffer", "elementwise"):
+    for key in ("mat_fwd_kernel", "bwd_prep_kernel", "zero_f32_kernel", "dq_finalize_kernel", "fwd_kernel",
+                "dkdv16_kernel", "dkdv_kernel", "dq_kernel", "copyBuffer", "elementwise"):
         if key in k:
+            if key == "dkdv16_kernel" and _template_args(k)[-2:] == ["false", "true"]:
+                return "atomic_dq_" + key
             if key in ("dkdv16_kernel", "dkdv_kernel", "dq_kernel") and _last_template_arg_true(k):
                 return "mat_" + key
             return key

@@ -108,6 +108,23 @@ def test_bwd_validation(L):
     assert call(wsb=1) == -5
 
 
+def test_atomic_validation(L):
+    assert L.attn_workspace_bytes_atomic(2, 3, 100, 64) == 2 * 3 * 100 * (64 * 4 + 8)
+    assert L.attn_workspace_bytes_atomic(1, 1, 1, 48) == 0
+
+    def call(dtype=0, ws=FAKE, wsb=1 << 30, **kw):
+        p = {k: FAKE for k in ("Q", "K", "V", "dO", "O", "L", "dQ", "dK", "dV")}
+        p.update(kw)
+        return L.attn_fwd_bwd_atomic(p["Q"], p["K"], p["V"], p["dO"], p["O"], p["L"], p["dQ"], p["dK"],
+                                     p["dV"], ws, wsb, 1, 2, 9, 64, 0.125, 1, dtype, None)
+    assert call(dtype=1) == -3            # bfloat16 only
+    assert call(ws=None) == -1
+    assert call(ws=FAKE + 4) == -4        # the accumulator needs 16-byte alignment
+    assert call(wsb=2 * 9 * (64 * 4 + 8) - 1) == -5
+    for name in ("Q", "K", "V", "dO", "O", "L", "dQ", "dK", "dV"):
+        assert call(**{name: None}) == -1, name
+
+
 def test_mat_bytes(L):
     # [B, H, n, lda] with lda = n rounded up to 128
     assert L.attn_mat_bytes(2, 3, 100, 0) == 2 * 3 * 100 * 128 * 2
