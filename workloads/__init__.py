@@ -22,7 +22,8 @@ import numpy as np
 
 __all__ = ["Workload", "WORKLOADS", "Inputs", "generate", "to_torch", "f32_to_bf16_bits",
            "bf16_bits_to_f32", "round_to_bf16", "causal_pairs", "alg_flops",
-           "alg_bytes"]
+           "alg_bytes", "DecodeWorkload", "DECODE_WORKLOADS", "DecodeInputs", "generate_decode",
+           "decode_to_torch", "decode_bytes"]
 
 
 @dataclass(frozen=True)
@@ -170,3 +171,111 @@ def alg_bytes(B: int, H: int, n: int, d: int, elem_bytes: int, fwd_only: bool = 
     if fwd_only:
         return B * H * (4 * n * d * elem_bytes + 4 * n)
     return B * H * (8 * n * d * elem_bytes + 4 * n)
+
+
+# ----------------------------------------------------------------- decode --
+@dataclass(frozen=True)
+class DecodeWorkload:
+    """One decode step: B sequences, Hq query heads over Hkv cache heads
+    (Hq / Hkv query heads per cache head), ``n`` tokens already cached per
+    sequence (or, with ``ragged``, between n/2 and n), a cache of capacity
+    n_cap rows, head dimension d. The new token's key and value are appended
+    at row len_b before it attends."""
+    name: str
+    B: int
+    Hq: int
+    Hkv: int
+    n: int
+    n_cap: int
+    d: int
+    dtype: str
+    ragged: bool
+    sigma_qk: float
+    seed: int
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.d)
+
+    @property
+    def elem_bytes(self) -> int:
+        return 4 if self.dtype == "f32" else 2
+
+
+# Decode workloads: a GQA serving batch (8 query heads per cache head), a long
+# single-sequence context, and the paper's shape (B = 2, one head per cache
+# head, d = 64, float32) at its largest cache length.
+DECODE_WORKLOADS: Dict[str, DecodeWorkload] = {w.name: w for w in [
+    DecodeWorkload("dec_b16_hq64_hkv8_n8192_d128_bf16", 16, 64, 8, 8192, 8193, 128, "bf16", False, 1.0, 11),
+    DecodeWorkload("dec_b1_hq64_hkv8_n131072_d128_bf16", 1, 64, 8, 131072, 131073, 128, "bf16", False, 1.0, 12),
+    DecodeWorkload("dec_b32_hq32_hkv8_n4096_d128_bf16_ragged", 32, 32, 8, 4096, 4097, 128, "bf16", True, 1.0, 13),
+    DecodeWorkload("dec_b2_h1_n1048576_d64_f32", 2, 1, 1, 1048576, 1048577, 64, "f32", False, 1.0, 14),
+]}
+
+
+@dataclass
+class DecodeInputs:
+    """q [B, Hq, d]; caches [B, Hkv, n_cap, d] (rows past a sequence's length
+    hold random values the step must ignore); k_new, v_new [B, Hkv, d]; lens
+    [B] int32 (tokens cached before the step). float32 arrays hold exactly
+    the values handed to the GPU; ``bits`` their bfloat16 patterns."""
+    workload: DecodeWorkload
+    q: np.ndarray
+    k_cache: np.ndarray
+    v_cache: np.ndarray
+    k_new: np.ndarray
+    v_new: np.ndarray
+    lens: np.ndarray
+    bits: Optional[Dict[str, np.ndarray]] = None
+
+
+def generate_decode(w: DecodeWorkload, *, n: Optional[int] = None, B: Optional[int] = None,
+                    seed: Optional[int] = None) -> DecodeInputs:
+    """Draw one decode step's inputs: one PCG64 stream per array, spawned from
+    SeedSequence(seed) in the order q, k_cache, v_cache, k_new, v_new, lens;
+    standard normal (q and keys times sigma_qk), bfloat16-rounded for bf16."""
+    B = w.B if B is None else B
+    n = w.n if n is None else n
+    n_cap = max(w.n_cap, n + 1)
+    seed = w.seed if seed is None else seed
+    shapes = {"q": (B, w.Hq, w.d), "k_cache": (B, w.Hkv, n_cap, w.d), "v_cache": (B, w.Hkv, n_cap, w.d),
+              "k_new": (B, w.Hkv, w.d), "v_new": (B, w.Hkv, w.d)}
+    sig = {"q": w.sigma_qk, "k_cache": w.sigma_qk, "k_new": w.sigma_qk, "v_cache": 1.0, "v_new": 1.0}
+    streams = np.random.SeedSequence(seed).spawn(6)
+    out, bits = {}, ({} if w.dtype == "bf16" else None)
+    for (name, shape), ss in zip(shapes.items(), streams[:5]):
+        x = np.random.Generator(np.random.PCG64(ss)).standard_normal(shape, dtype=np.float32)
+        if sig[name] != 1.0:
+            x *= np.float32(sig[name])
+        if bits is not None:
+            bb = f32_to_bf16_bits(x)
+            bits[name] = bb
+            x = bf16_bits_to_f32(bb)
+        out[name] = x
+    g = np.random.Generator(np.random.PCG64(streams[5]))
+    lens = g.integers(max(n // 2, 0), n + 1, size=B).astype(np.int32) if w.ragged else \
+        np.full(B, n, dtype=np.int32)
+    return DecodeInputs(w, out["q"], out["k_cache"], out["v_cache"], out["k_new"], out["v_new"], lens, bits)
+
+
+def decode_to_torch(inp: DecodeInputs, device="cuda") -> Dict[str, "object"]:
+    import torch
+    out = {}
+    for name in ("q", "k_cache", "v_cache", "k_new", "v_new"):
+        if inp.workload.dtype == "bf16":
+            out[name] = torch.from_numpy(inp.bits[name].view(np.int16)).to(device).view(torch.bfloat16)
+        else:
+            out[name] = torch.from_numpy(getattr(inp, name)).to(device)
+    out["lens"] = torch.from_numpy(inp.lens).to(device)
+    return out
+
+
+def decode_bytes(lens, Hq: int, Hkv: int, d: int, elem_bytes: int, append: bool = True) -> int:
+    """Minimum HBM bytes of one decode step: every cached key and value row
+    the step attends to read once (the appended row written once), q read and
+    O written once, L written (float32)."""
+    B = len(lens)
+    rows = sum(int(x) for x in lens)
+    kv = 2 * Hkv * d * elem_bytes * rows
+    new = 2 * 2 * B * Hkv * d * elem_bytes if append else 0     # k_new/v_new read, cache row written
+    return kv + new + 2 * B * Hq * d * elem_bytes + 4 * B * Hq
