@@ -4,6 +4,8 @@
     python bench.py --mode fwd|bwd      attn_fwd or attn_bwd alone
     python bench.py --mode naive        fused versus the naive materialising path
     python bench.py --mode atomic       attn_fwd_bwd versus the atomic-dQ variant
+    python bench.py --mode decode [--decode-workload NAME] [--decode-sweep]
+                                        one decode step over a KV cache (HBM-bound)
 
 One step is one attn_fwd_bwd call (forward, dK/dV and dQ kernels) over the
 whole workload, inputs resident in HBM before timing starts. Prints ONE JSON
@@ -292,6 +294,82 @@ def bench_atomic(args, w, inp, dev, out, ws, hip, torch, attn) -> int:
     return 0
 
 
+def bench_decode(args, torch, attn, hip) -> int:
+    """One decode step (append the new token, attend over the cache) timed on
+    resident inputs; the step is HBM-bound, so the roofline is bytes per second
+    against the 8 TB/s peak. --decode-sweep times the step over cache lengths
+    1024 ... 2^20 (the paper's sweep) and reports the local scaling exponent."""
+    w = workloads.DECODE_WORKLOADS[args.decode_workload]
+    print(f"[bench] decode workload {w.name}: generating seeded inputs", file=sys.stderr, flush=True)
+
+    def setup(n=None, B=None):
+        inp = workloads.generate_decode(w, n=n, B=B)
+        dev = workloads.decode_to_torch(inp, "cuda")
+        n_max = int(inp.lens.max())
+        ws_b = attn.attn_decode_workspace_bytes(len(inp.lens), w.Hq, w.Hkv, n_max, w.d, True)
+        ws = torch.empty(max(ws_b, 16), dtype=torch.uint8, device="cuda")
+        O = torch.empty_like(dev["q"])
+        L = torch.empty(dev["q"].shape[:2], dtype=torch.float32, device="cuda")
+        call = lambda: attn.attn_decode(dev["q"], dev["k_cache"], dev["v_cache"], dev["k_new"], dev["v_new"],
+                                        cache_lens=dev["lens"], n=n_max, scale=w.scale, out=(O, L),
+                                        workspace=ws)
+        return inp, dev, call, O, L
+
+    if args.decode_sweep:
+        rows = []
+        n = 1024
+        while n <= 1 << 20:
+            inp, dev, call, O, L = setup(n=n)
+            t = _time_calls(call, args.steps, args.warmup, hip, torch)
+            nbytes = workloads.decode_bytes(inp.lens, w.Hq, w.Hkv, w.d, w.elem_bytes)
+            rows.append((n, t[0], nbytes / (t[0] * 1e-3) / 1e9))
+            del inp, dev
+            torch.cuda.empty_cache()
+            n *= 4
+        expo = [round(np.log(rows[i + 1][1] / rows[i][1]) / np.log(rows[i + 1][0] / rows[i][0]), 3)
+                for i in range(len(rows) - 1)]
+        print(json.dumps({"metric": "decode step time versus cache length (1 GPU)", "workload": w.name,
+                          "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "d": w.d, "dtype": w.dtype,
+                          "points": [{"n": r[0], "ms": round(r[1], 5), "GB/s": round(r[2], 1)} for r in rows],
+                          "local_exponent": expo}), flush=True)
+        return 0
+
+    inp, dev, call, O, L = setup()
+    t = _time_calls(call, args.steps, args.warmup, hip, torch)
+    B = len(inp.lens)
+    nbytes = workloads.decode_bytes(inp.lens, w.Hq, w.Hkv, w.d, w.elem_bytes)
+    gbs = nbytes / (t[0] * 1e-3) / 1e9
+    rec = {
+        "metric": "decode step HBM bandwidth (1 GPU)", "value": round(gbs, 1), "unit": "GB/s",
+        "higher_is_better": True, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(t[1], 5), "device_ms_per_step": round(t[0], 5), "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "tokens_per_s": round(B / (t[0] * 1e-3), 1),
+        "config": {"workload": w.name, "B": B, "Hq": w.Hq, "Hkv": w.Hkv, "n": w.n, "d": w.d,
+                   "ragged": w.ragged, "alg_bytes": nbytes},
+        "roofline": {"kernel": "attn_decode (whole call)", "bound": "hbm", "achieved": round(gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import decode as dec
+        torch.cuda.synchronize()
+        bs = list(range(min(B, 2)))
+        c0 = time.perf_counter()
+        ref = dec.decode_step(inp.q[bs], inp.k_cache[bs], inp.v_cache[bs], inp.lens[bs], w.scale,
+                              inp.k_new[bs], inp.v_new[bs])
+        t_cpu = time.perf_counter() - c0
+        import oracle
+        rec["max_rel_err"] = {
+            "O": float(f"{oracle.max_rel_err(O[bs].float().cpu().numpy(), ref['O']):.3e}"),
+            "L": float(f"{oracle.max_rel_err(L[bs].cpu().numpy(), ref['L']):.3e}")}
+        sample_bytes = workloads.decode_bytes(inp.lens[bs], w.Hq, w.Hkv, w.d, w.elem_bytes)
+        rec["cpu_baseline"] = {"value": round(sample_bytes / t_cpu / 1e9, 3), "unit": "GB/s", "cores": cpu_threads(),
+                               "kind": "oracle",
+                               "sample": f"{len(bs)} of {B} sequences, float64 NumPy decode step, {t_cpu:.1f} s"}
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
 def measured_traffic_kernel(workload: str, kernel: str, prefix: str = "hbm_traffic"):
     """fetch/write bytes per launch of `kernel` from a committed summary, or None."""
     from paper_2609_33916_amd import profiling
@@ -307,7 +385,11 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(workloads.WORKLOADS))
-    ap.add_argument("--mode", default="fwd_bwd", choices=("fwd_bwd", "fwd", "bwd", "naive", "atomic"),
+    ap.add_argument("--decode-workload", default="dec_b16_hq64_hkv8_n8192_d128_bf16",
+                    choices=sorted(workloads.DECODE_WORKLOADS))
+    ap.add_argument("--decode-sweep", action="store_true",
+                    help="with --mode decode: time cache lengths 1024 ... 2^20 of the workload's shape")
+    ap.add_argument("--mode", default="fwd_bwd", choices=("fwd_bwd", "fwd", "bwd", "naive", "atomic", "decode"),
                     help="entry point timed: attn_fwd_bwd (default), attn_fwd, attn_bwd, or the "
                          "fused path against the naive materialising path")
     ap.add_argument("--no-cpu-baseline", action="store_true",
@@ -338,6 +420,8 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": nbytes, "copies": 5}), flush=True)
         return 0
+    if args.mode == "decode":
+        return bench_decode(args, torch, attn, HipEvents())
     w = workloads.WORKLOADS[args.workload]
     print(f"[bench] workload {w.name}: generating seeded inputs", file=sys.stderr, flush=True)
     inp = workloads.generate(w)

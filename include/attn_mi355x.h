@@ -187,6 +187,36 @@ int attn_mat_fwd_bwd(const void* Q, const void* K, const void* V, const void* dO
                      int B, int H, int n, int d, float scale, int causal, int dtype,
                      void* stream);
 
+/* ---- Decode (Paper III) -------------------------------------------------
+ * One decode step over a KV cache: for every sequence b the new token's key
+ * and value are appended at row len_b of its cache head (when k_new/v_new are
+ * given), and its query heads attend to the first T_b = len_b + 1 rows (len_b
+ * without an append):
+ *   O[b,h] = softmax_j(scale q[b,h] . K[b,g,j]) V[b,g,j],  g = h / (Hq/Hkv)
+ *   L[b,h] = ln sum_j exp(scale q[b,h] . K[b,g,j])
+ * Grouped-query attention: Hq query heads share Hkv cache heads (Hq a multiple
+ * of Hkv; Hkv = 1 is multi-query attention). A step with no key writes O = 0
+ * and L = -inf.
+ *
+ * Layout: q, O [B, Hq, d]; k_cache, v_cache [B, Hkv, n_cap, d] (row j of a
+ * cache head is token j); k_new, v_new [B, Hkv, d]; L float32 [B, Hq] or NULL;
+ * cache_lens: device int32 [B] (len_b, clamped to [0, n]) or NULL (every len_b
+ * = n). n_cap >= n + 1 with an append, >= n without. bfloat16 only
+ * (ATTN_E_UNSUPPORTED for float32). The caches are written only at row len_b.
+ *
+ * Work split: a workgroup owns one cache head, one split of its keys and up to
+ * 32 of the query heads that read it, so each cache row is read once per
+ * step; the keys are split (n + 1 rounded to 128-key tiles) until there are
+ * about 512 workgroups, and a last pass merges the splits by log-sum-exp. The
+ * merge needs attn_decode_workspace_bytes(...) bytes of 16-byte aligned
+ * workspace (0 when the keys are not split; workspace may then be NULL). */
+size_t attn_decode_workspace_bytes(int B, int Hq, int Hkv, int n, int d, int append);
+
+int attn_decode(const void* q, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                const int* cache_lens, void* O, float* L, void* workspace, size_t workspace_bytes,
+                int B, int Hq, int Hkv, int n, int n_cap, int d, float scale, int dtype,
+                void* stream);
+
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* attn_strerror(int code);
 

@@ -26,7 +26,7 @@ import torch  # loads the process's HIP runtime before the library
 
 __all__ = ["attn_fwd", "attn_fwd_bwd", "attn_fwd_bwd_timed", "attn_bwd", "attn_workspace_bytes", "attn_strerror",
            "attn_mat_bytes", "attn_mat_lda", "attn_mat_fwd", "attn_mat_bwd", "attn_mat_fwd_bwd",
-           "attn_fwd_bwd_atomic", "attn_workspace_bytes_atomic",
+           "attn_fwd_bwd_atomic", "attn_workspace_bytes_atomic", "attn_decode", "attn_decode_workspace_bytes",
            "AttnError", "lib", "LIB_PATH", "ATTN_BF16", "ATTN_F32"]
 
 # ATTN_MI355X_LIB may name another build of the same library (A/B comparison
@@ -66,6 +66,10 @@ def lib() -> ctypes.CDLL:
     L.attn_fwd_bwd_timed.restype = i
     L.attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, f, i, i, vp]
     L.attn_bwd.restype = i
+    L.attn_decode_workspace_bytes.argtypes = [i, i, i, i, i, i]
+    L.attn_decode_workspace_bytes.restype = sz
+    L.attn_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, i, i, f, i, vp]
+    L.attn_decode.restype = i
     L.attn_workspace_bytes_atomic.argtypes = [i, i, i, i]
     L.attn_workspace_bytes_atomic.restype = sz
     L.attn_fwd_bwd_atomic.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
@@ -341,3 +345,56 @@ def attn_fwd_bwd_atomic(q, k, v, do, scale: Optional[float] = None, causal: bool
     if rc != 0:
         raise AttnError(rc, "attn_fwd_bwd_atomic")
     return O, L, dQ, dK, dV
+
+
+# --------------------------------------------------------------- decode --
+def attn_decode_workspace_bytes(B: int, Hq: int, Hkv: int, n: int, d: int, append: bool = True) -> int:
+    return int(lib().attn_decode_workspace_bytes(B, Hq, Hkv, n, d, int(bool(append))))
+
+
+def attn_decode(q, k_cache, v_cache, k_new=None, v_new=None, cache_lens=None, n: Optional[int] = None,
+                scale: Optional[float] = None, out=None, workspace=None):
+    """One decode step: appends k_new/v_new ([B, Hkv, d]) at row cache_lens[b]
+    of the caches ([B, Hkv, n_cap, d], updated in place) and attends q
+    ([B, Hq, d]) to the first cache_lens[b] + 1 rows. cache_lens is an int32
+    GPU tensor [B] or None (every sequence holds n tokens). Returns (O, L)."""
+    if q.dim() != 3 or k_cache.dim() != 4:
+        raise ValueError("q must be [B, Hq, d] and the caches [B, Hkv, n_cap, d]")
+    B, Hq, d = q.shape
+    Hkv, n_cap = k_cache.shape[1], k_cache.shape[2]
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache)):
+        if not t.is_cuda or t.dtype != q.dtype or tuple(t.shape) != (B, Hkv, n_cap, d) or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous GPU tensor [B, Hkv, n_cap, d] of q's dtype")
+    if not q.is_cuda or not q.is_contiguous():
+        raise ValueError("q must be a contiguous GPU tensor")
+    append = k_new is not None
+    if append:
+        for name, t in (("k_new", k_new), ("v_new", v_new)):
+            if t is None or not t.is_cuda or t.dtype != q.dtype or tuple(t.shape) != (B, Hkv, d) \
+                    or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous GPU tensor [B, Hkv, d] of q's dtype")
+    if cache_lens is not None:
+        if not cache_lens.is_cuda or cache_lens.dtype != torch.int32 or tuple(cache_lens.shape) != (B,):
+            raise ValueError("cache_lens must be an int32 GPU tensor [B]")
+    if n is None:
+        if cache_lens is None:
+            raise ValueError("n is required without cache_lens")
+        n = int(cache_lens.max().item())
+    if out is None:
+        O = torch.empty_like(q)
+        L = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    else:
+        O, L = out
+    wsb = attn_decode_workspace_bytes(B, Hq, Hkv, n, d, append)
+    if workspace is None and wsb > 0:
+        workspace = torch.empty(wsb, dtype=torch.uint8, device=q.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    rc = lib().attn_decode(q.data_ptr(), k_new.data_ptr() if append else None,
+                           v_new.data_ptr() if append else None, k_cache.data_ptr(), v_cache.data_ptr(),
+                           cache_lens.data_ptr() if cache_lens is not None else None,
+                           O.data_ptr(), L.data_ptr() if L is not None else None, ws_ptr, ws_len,
+                           B, Hq, Hkv, n, n_cap, d, _scale(scale, d), _dtype_code(q), _stream(q.device))
+    if rc != 0:
+        raise AttnError(rc, "attn_decode")
+    return O, L

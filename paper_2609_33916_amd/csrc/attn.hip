@@ -4,6 +4,7 @@
 // error code can be exercised without a GPU.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <limits>
@@ -141,6 +142,28 @@ template <template <typename, int, bool> class F, typename Args>
 void run_dispatch(int dtype, int d, int causal, Args a, int heads, hipStream_t st) {
   if (dtype == ATTN_BF16) by_d<F, bf16>(d, causal, a, heads, st);
   else by_d<F, float>(d, causal, a, heads, st);
+}
+
+// Decode: split plan. A workgroup owns (batch, cache head, up to 32 query
+// heads, one split of the keys); the keys are split until there are about two
+// workgroups per compute unit, each split a whole number of 128-key tiles.
+struct DecodePlan {
+  int qchunks, nsplit, chunk;
+};
+constexpr int kDecodeTargetWGs = 512;
+DecodePlan decode_plan(int B, int Hq, int Hkv, int n, int append) {
+  DecodePlan p;
+  const int G = Hq / Hkv;
+  p.qchunks = (G + 31) / 32;
+  const long long groups = (long long)B * Hkv * p.qchunks;
+  const long long keys = (long long)n + append;
+  const long long tiles = std::max<long long>(1, (keys + 127) / 128);
+  long long ns = std::max<long long>(1, (kDecodeTargetWGs + groups - 1) / groups);
+  ns = std::min(ns, tiles);
+  const long long per = (tiles + ns - 1) / ns;     // tiles per split
+  p.chunk = (int)(per * 128);
+  p.nsplit = (int)((tiles + per - 1) / per);
+  return p;
 }
 
 // Row stride of the materialised attention matrix: n rounded up to a
@@ -476,6 +499,72 @@ int attn_fwd_bwd_atomic(const void* Q, const void* K, const void* V, const void*
 
   hipLaunchKernelGGL((attn::dq_finalize_kernel<bf16>), dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, st,
                      dqacc, static_cast<bf16*>(dQ), n8, scale);
+  if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
+  return ATTN_OK;
+}
+
+size_t attn_decode_workspace_bytes(int B, int Hq, int Hkv, int n, int d, int append) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || n < 0 || (d != 32 && d != 64 && d != 128)) return 0;
+  const DecodePlan p = decode_plan(B, Hq, Hkv, n, append ? 1 : 0);
+  if (p.nsplit == 1) return 0;
+  return (size_t)B * Hq * p.nsplit * (size_t)(d + 2) * sizeof(float);
+}
+
+int attn_decode(const void* q, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                const int* cache_lens, void* O, float* L, void* workspace, size_t workspace_bytes,
+                int B, int Hq, int Hkv, int n, int n_cap, int d, float scale, int dtype, void* stream) {
+  if (!q || !k_cache || !v_cache || !O) return ATTN_E_NULL;
+  if ((k_new == nullptr) != (v_new == nullptr)) return ATTN_E_NULL;
+  const int append = k_new ? 1 : 0;
+  if (B < 1 || Hq < 1 || Hkv < 1 || n < 0 || n_cap < 1 || n_cap < n + append) return ATTN_E_SHAPE;
+  if (Hq % Hkv != 0) return ATTN_E_SHAPE;
+  if (dtype != ATTN_BF16 && dtype != ATTN_F32) return ATTN_E_UNSUPPORTED;
+  if (dtype != ATTN_BF16) return ATTN_E_UNSUPPORTED;
+  if (d != 32 && d != 64 && d != 128) return ATTN_E_UNSUPPORTED;
+  if (!std::isfinite(scale)) return ATTN_E_ARG;
+  if ((long long)B * Hkv * (long long)n_cap * d > (1LL << 46)) return ATTN_E_SHAPE;
+  if ((long long)B * Hq * Hkv > std::numeric_limits<int>::max()) return ATTN_E_SHAPE;
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(O, 16) ||
+      (k_new && (!aligned(k_new, 16) || !aligned(v_new, 16))) || (L && !aligned(L, 4)) ||
+      (cache_lens && !aligned(cache_lens, 4)))
+    return ATTN_E_ALIGN;
+  const DecodePlan plan = decode_plan(B, Hq, Hkv, n, append);
+  const size_t need = attn_decode_workspace_bytes(B, Hq, Hkv, n, d, append);
+  if (need > 0) {
+    if (!workspace) return ATTN_E_NULL;
+    if (!aligned(workspace, 16)) return ATTN_E_ALIGN;
+    if (workspace_bytes < need) return ATTN_E_WORKSPACE;
+  }
+  if ((long long)B * Hkv * plan.qchunks > 65535) return ATTN_E_SHAPE;   // grid y limit
+  const ScaleParts sp = split_scale(scale, dtype);
+  attn::DecArgs a{};
+  a.q = q; a.kc = k_cache; a.vc = v_cache; a.k_new = k_new; a.v_new = v_new;
+  a.lens = cache_lens;
+  a.part = static_cast<float*>(workspace);
+  a.o = O; a.lse = L;
+  a.rows = B * Hq;
+  a.Hq = Hq; a.Hkv = Hkv; a.G = Hq / Hkv; a.n = n; a.n_cap = n_cap; a.append = append;
+  a.chunk = plan.chunk; a.nsplit = plan.nsplit; a.qchunks = plan.qchunks;
+  a.sl2 = sp.sl2;
+  a.qflip = sp.qflip;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  const dim3 grid(plan.nsplit, B * Hkv * plan.qchunks);
+  auto launch = [&](auto dtag) {
+    constexpr int D = decltype(dtag)::value;
+    if (append) {
+      const long long chunks = 2LL * B * Hkv * (D / 8);
+      hipLaunchKernelGGL((attn::decode_append_kernel<bf16, D>), dim3((unsigned)((chunks + 255) / 256)), dim3(256),
+                         0, st, a, B);
+    }
+    hipLaunchKernelGGL((attn::decode_kernel<D>), grid, dim3(256), 0, st, a);
+    if (plan.nsplit > 1)
+      hipLaunchKernelGGL((attn::decode_combine_kernel<bf16, D>), dim3((unsigned)((B * Hq + 3) / 4)), dim3(256), 0,
+                         st, a.part, O, L, B * Hq, plan.nsplit);
+  };
+  if (d == 32) launch(std::integral_constant<int, 32>{});
+  else if (d == 64) launch(std::integral_constant<int, 64>{});
+  else launch(std::integral_constant<int, 128>{});
   if (hipGetLastError() != hipSuccess) return ATTN_E_HIP;
   return ATTN_OK;
 }

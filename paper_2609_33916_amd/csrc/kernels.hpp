@@ -1091,6 +1091,261 @@ __global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
 }
 
 // ======================================================================
+// Decode (Paper III): one new query token per head against a KV cache.
+//
+// decode_append_kernel writes the new token's key and value at row len_b of
+// its cache head. decode_kernel then covers keys [0, T_b) of every cache head
+// (T_b = len_b + 1 with an append): a workgroup owns one cache head, one
+// split of the keys (``chunk`` keys, a multiple of 128) and up to 32 of the
+// query heads that share the cache head (GQA; MQA when there is one cache
+// head), so K and V are read once for the whole group. The group's queries
+// are the 32 columns of S^T = K Q^T (missing heads are zero columns); each
+// wave takes one 32-key block of every 128-key tile with its own online
+// softmax (base 2), the waves' partial (max, sum, O) are merged through LDS
+// at the end, and with several splits decode_combine_kernel merges the
+// splits by their log-sum-exp.
+// ======================================================================
+struct DecArgs {
+  const void* q;        // [B, Hq, d]
+  const void* kc;       // [B, Hkv, n_cap, d]
+  const void* vc;
+  const void* k_new;    // [B, Hkv, d] or null
+  const void* v_new;
+  const int* lens;      // [B] tokens cached before the step, or null (all n)
+  float* part;          // splits > 1: [B*Hq][nsplit][d] unnormalised O, then [B*Hq][nsplit] (max2, sum)
+  void* o;              // [B, Hq, d]
+  float* lse;           // [B, Hq] natural log, or null
+  int rows;            // B * Hq
+  int Hq, Hkv, G, n, n_cap, append;
+  int chunk, nsplit, qchunks;
+  float sl2;
+  uint32_t qflip;
+};
+
+__device__ __forceinline__ int dec_len(const DecArgs& a, int b) {
+  const int len = a.lens ? a.lens[b] : a.n;
+  return min(max(len, 0), a.n);     // lengths are clamped to [0, n]
+}
+
+template <typename T, int D>
+__global__ void __launch_bounds__(256) decode_append_kernel(const DecArgs a, int B) {
+  constexpr int CH = Elem<T>::CH, CPR = D / CH;     // 16-byte chunks per row
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  const long long rows = (long long)B * a.Hkv;
+  if (i >= 2 * rows * CPR) return;
+  const int which = (int)(i / (rows * CPR));         // 0: key, 1: value
+  const long long r = (i / CPR) % rows;              // b * Hkv + hk
+  const int ch = (int)(i % CPR);
+  const int b = (int)(r / a.Hkv);
+  const int pos = dec_len(a, b);
+  const T* src = (const T*)(which ? a.v_new : a.k_new) + r * D + ch * CH;
+  T* dst = (T*)(which ? a.vc : a.kc) + (r * a.n_cap + pos) * D + ch * CH;
+  *(u32x4*)dst = *(const u32x4*)src;
+}
+
+template <int D>
+__global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
+  using T = bf16;
+  using E = Elem<T>;
+  using Frag = typename E::frag;
+  constexpr int BKV = 64, NKB = 2, NDB = D / 32;
+  constexpr int KP = E::KP, TD = D / (2 * KP), T32 = 16 / KP;
+  using TL = Tile<T, BKV, D>;
+  static_assert(BKV == 64, "TransRead reads 64-row tiles");
+  // two stages, each [K rows 0-63, K rows 64-127, V rows 0-63, V rows 64-127]
+  __shared__ __attribute__((aligned(16))) T stA[4][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) T stB[4][TL::ELEMS];
+
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int split = blockIdx.x;
+  const int grp = blockIdx.y;                        // (b, hk, qc)
+  const int qc = grp % a.qchunks;
+  const int bh = grp / a.qchunks;                    // b * Hkv + hk
+  const int b = bh / a.Hkv, hk = bh % a.Hkv;
+  const int T_b = dec_len(a, b) + a.append;
+  const int k_lo = split * a.chunk, k_hi = min(T_b, k_lo + a.chunk);
+  const int h0 = hk * a.G + qc * 32;                 // first query head of this workgroup
+  const int nq = min(32, a.G - qc * 32);             // query heads in it
+  const size_t kvoff = (size_t)bh * a.n_cap * D;
+  const T* Kg = (const T*)a.kc + kvoff;
+  const T* Vg = (const T*)a.vc + kvoff;
+  const T* Qg = (const T*)a.q + ((size_t)b * a.Hq + h0) * D;
+
+  RowFrags<T, D> qf;
+  qf.load(Qg, c, nq, h, a.qflip);
+  const float sl2 = a.sl2;
+  const int sub = w >> 1, kb = w & 1;                // this wave: sub-tile and 32-key block
+  const int nt = k_hi > k_lo ? (k_hi - k_lo + 127) / 128 : 0;
+
+  TileLoader<T, BKV, D> ld(w, lane);
+  auto issue = [&](T (&stg)[4][TL::ELEMS], int kv0) __attribute__((always_inline)) {
+    ld.issue(stg[0], Kg, kv0, k_hi, w);
+    ld.issue(stg[1], Kg, kv0 + 64, k_hi, w);
+    ld.issue(stg[2], Vg, kv0, k_hi, w);
+    ld.issue(stg[3], Vg, kv0 + 64, k_hi, w);
+  };
+  if (nt > 0) issue(stA, k_lo);
+  __syncthreads();
+
+  f32x16 oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = zero16();
+  float m_use = -INFINITY, lsum = 0.f;
+
+  auto step = [&](int it, T (&cur)[4][TL::ELEMS], T (&nxt)[4][TL::ELEMS]) __attribute__((always_inline)) {
+    const int kv0 = k_lo + it * 128;
+    if (it + 1 < nt) issue(nxt, kv0 + 128);
+    const int kb0 = kv0 + 64 * sub + 32 * kb;        // first key of this wave's block
+    if (kb0 < k_hi) {
+      const T* kl = cur[sub];
+      const T* vl = cur[2 + sub];
+      f32x16 s = zero16();
+#pragma unroll
+      for (int t = 0; t < TD; ++t) mma(s, RowRead<T, D>::get(kl, kb, t, h, c), qf.f[t]);
+      // lane (h, c): s[j] = raw score of key kb0 + 16h + j for query column c
+      if (kb0 + 32 > k_hi) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (kb0 + 16 * h + j >= k_hi) s[j] = -INFINITY;
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[j]);
+      const float mt = halves_max(mx) * sl2;
+      const bool resc = mt > m_use + kRescaleThresh;
+      if (__builtin_amdgcn_ballot_w64(resc)) {
+        const float alpha = resc ? exp2_fast(m_use - mt) : 1.f;
+        if (resc) m_use = mt;
+        lsum *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
+      }
+      const float mb = (m_use == -INFINITY) ? 0.f : -m_use;
+      float rs = 0.f;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const float p = exp2_fast(fmaf(s[j], sl2, mb));
+        rs += p;
+        s[j] = p;
+      }
+      lsum += rs;
+#pragma unroll
+      for (int t = 0; t < T32; ++t) {
+        const Frag pf = FragFromAcc<T>::get(s, t);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) mma(oacc[db], TransRead<T, D>::get(vl, kb, db, t, h, c), pf);
+      }
+    }
+    __syncthreads();
+  };
+  for (int it = 0; it < nt; it += 2) {
+    step(it, stA, stB);
+    if (it + 1 < nt) step(it + 1, stB, stA);
+  }
+
+  // ---- merge the four waves through LDS (the stage memory is free now):
+  // O parts [4][D][32] in stA, maxima and sums [4][32] each in stB
+  float* ow = (float*)&stA[0][0];
+  float* mw = (float*)&stB[0][0];
+  float* lw = mw + 4 * 32;
+  static_assert(4 * D * 32 * 4 <= 4 * TL::ELEMS * 2, "merge buffer exceeds the stage");
+  const float ltot = halves_sum(lsum);
+  if (h == 0) {
+    mw[w * 32 + c] = m_use;
+    lw[w * 32 + c] = ltot;
+  }
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int dd = 32 * db + 8 * (j >> 2) + 4 * h + (j & 3);
+      ow[(w * D + dd) * 32 + c] = oacc[db][j];
+    }
+  __syncthreads();
+  // thread -> query column qq and D/8 consecutive d values
+  const int qq = tid & 31, dpart = tid >> 5;
+  constexpr int DPT = D / 8;
+  float M = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) M = fmaxf(M, mw[v * 32 + qq]);
+  float f[4], l = 0.f;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    f[v] = (M == -INFINITY) ? 0.f : exp2_fast(mw[v * 32 + qq] - M);
+    l += f[v] * lw[v * 32 + qq];
+  }
+  if (qq < nq) {
+    const size_t row = (size_t)b * a.Hq + h0 + qq;
+    float r[DPT];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) {
+      const int dd = dpart * DPT + e;
+      float acc = 0.f;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc += f[v] * ow[(v * D + dd) * 32 + qq];
+      r[e] = acc;
+    }
+    if (a.nsplit == 1) {
+      const float inv = l > 0.f ? 1.f / l : 0.f;
+      T* Og = (T*)a.o + row * D + dpart * DPT;
+#pragma unroll
+      for (int e4 = 0; e4 < DPT / 4; ++e4)
+        Quad<T>::store(Og + 4 * e4, r[4 * e4] * inv, r[4 * e4 + 1] * inv, r[4 * e4 + 2] * inv, r[4 * e4 + 3] * inv);
+      if (a.lse && dpart == 0) a.lse[row] = l > 0.f ? (M + log2f(l)) * kLn2 : -INFINITY;
+    } else {
+      // partials: [rows][nsplit][D] unnormalised O, then [rows][nsplit] (max2, sum)
+      float* pml = a.part + (size_t)a.rows * a.nsplit * D + (row * a.nsplit + split) * 2;
+      if (dpart == 0) {
+        pml[0] = M;
+        pml[1] = l;
+      }
+      float* po = a.part + (row * a.nsplit + split) * D + dpart * DPT;
+#pragma unroll
+      for (int e4 = 0; e4 < DPT / 4; ++e4)
+        *(f32x4*)(po + 4 * e4) = (f32x4){r[4 * e4], r[4 * e4 + 1], r[4 * e4 + 2], r[4 * e4 + 3]};
+    }
+  }
+}
+
+// Merge the splits of decode_kernel: per (b, query head), O = sum_s 2^(m_s - M)
+// O_s / sum_s 2^(m_s - M) l_s and L = (M + log2 l) ln 2. One wave per row.
+template <typename T, int D>
+__global__ void __launch_bounds__(256) decode_combine_kernel(const float* part, void* o, float* lse, int rows,
+                                                             int nsplit) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float* po = part + (size_t)row * nsplit * D;
+  const float* pml = part + (size_t)rows * nsplit * D + (size_t)row * nsplit * 2;
+  float M = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, pml[2 * s]);
+  float l = 0.f;
+  constexpr int DPL = D / 64 > 0 ? D / 64 : 1;       // d values per lane
+  float acc[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const float f = (M == -INFINITY) ? 0.f : exp2_fast(pml[2 * s] - M);
+    l += f * pml[2 * s + 1];
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) {
+      const int dd = lane + 64 * e;
+      if (dd < D) acc[e] += f * po[(size_t)s * D + dd];
+    }
+  }
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  T* O = (T*)o + (size_t)row * D;
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) {
+    const int dd = lane + 64 * e;
+    if (dd < D) O[dd] = (T)(acc[e] * inv);
+  }
+  if (lse && lane == 0) lse[row] = l > 0.f ? (M + log2f(l)) * kLn2 : -INFINITY;
+}
+
+// ======================================================================
 // Atomic-dQ support: zero the float32 accumulator, then dQ = scale * acc in
 // the output dtype. HBM-bound, 8 elements per thread.
 // ======================================================================

@@ -125,6 +125,36 @@ def test_atomic_validation(L):
         assert call(**{name: None}) == -1, name
 
 
+def test_decode_validation(L):
+    # no split at 300 keys for 16 groups? workspace only when the keys are split
+    assert L.attn_decode_workspace_bytes(1, 8, 1, 50000, 128, 1) > 0
+    assert L.attn_decode_workspace_bytes(64, 64, 8, 100, 128, 1) == 0
+    assert L.attn_decode_workspace_bytes(1, 6, 4, 10, 64, 1) == 0      # 6 % 4 != 0: invalid
+
+    def call(q=FAKE, kn=FAKE, vn=FAKE, kc=FAKE, vc=FAKE, lens=None, o=FAKE, lse=FAKE, ws=FAKE, wsb=1 << 30,
+             B=2, Hq=8, Hkv=2, n=10, n_cap=11, d=64, scale=0.125, dtype=0):
+        return L.attn_decode(q, kn, vn, kc, vc, lens, o, lse, ws, wsb, B, Hq, Hkv, n, n_cap, d, scale, dtype, None)
+    assert call(q=None) == -1
+    assert call(kc=None) == -1
+    assert call(o=None) == -1
+    assert call(kn=None) == -1             # k_new without v_new
+    assert call(n_cap=10) == -2           # no room for the appended row
+    assert call(kn=None, vn=None, n_cap=9) == -2    # without an append n_cap must still hold n rows
+    assert call(Hq=6, Hkv=4) == -2
+    assert call(Hkv=0) == -2
+    assert call(n=-1) == -2
+    assert call(d=80) == -3
+    assert call(dtype=1) == -3            # bfloat16 only
+    assert call(scale=float("nan")) == -7
+    assert call(q=MIS) == -4
+    assert call(lens=FAKE + 2) == -4
+    assert call(lse=FAKE + 2) == -4
+    big = dict(B=1, Hq=8, Hkv=1, n=50000, n_cap=50001, d=128)
+    assert call(ws=None, **big) == -1
+    assert call(ws=FAKE + 4, **big) == -4
+    assert call(wsb=16, **big) == -5
+
+
 def test_mat_bytes(L):
     # [B, H, n, lda] with lda = n rounded up to 128
     assert L.attn_mat_bytes(2, 3, 100, 0) == 2 * 3 * 100 * 128 * 2

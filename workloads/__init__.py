@@ -203,13 +203,13 @@ class DecodeWorkload:
 
 
 # Decode workloads: a GQA serving batch (8 query heads per cache head), a long
-# single-sequence context, and the paper's shape (B = 2, one head per cache
-# head, d = 64, float32) at its largest cache length.
+# single-sequence context, a ragged batch, and the paper's sizes (B = 2, one
+# head, d = 64; the paper runs them in float32) at its largest cache length.
 DECODE_WORKLOADS: Dict[str, DecodeWorkload] = {w.name: w for w in [
     DecodeWorkload("dec_b16_hq64_hkv8_n8192_d128_bf16", 16, 64, 8, 8192, 8193, 128, "bf16", False, 1.0, 11),
     DecodeWorkload("dec_b1_hq64_hkv8_n131072_d128_bf16", 1, 64, 8, 131072, 131073, 128, "bf16", False, 1.0, 12),
     DecodeWorkload("dec_b32_hq32_hkv8_n4096_d128_bf16_ragged", 32, 32, 8, 4096, 4097, 128, "bf16", True, 1.0, 13),
-    DecodeWorkload("dec_b2_h1_n1048576_d64_f32", 2, 1, 1, 1048576, 1048577, 64, "f32", False, 1.0, 14),
+    DecodeWorkload("dec_b2_h1_n1048576_d64_bf16", 2, 1, 1, 1048576, 1048577, 64, "bf16", False, 1.0, 14),
 ]}
 
 
