@@ -550,16 +550,17 @@ int attn_decode(const void* q, const void* k_new, const void* v_new, void* k_cac
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   const dim3 grid(plan.nsplit, B * Hkv * plan.qchunks);
+  a.fuse_append = append && plan.qchunks == 1;
   auto launch = [&](auto dtag) {
     constexpr int D = decltype(dtag)::value;
-    if (append) {
+    if (append && !a.fuse_append) {
       const long long chunks = 2LL * B * Hkv * (D / 8);
       hipLaunchKernelGGL((attn::decode_append_kernel<bf16, D>), dim3((unsigned)((chunks + 255) / 256)), dim3(256),
                          0, st, a, B);
     }
     hipLaunchKernelGGL((attn::decode_kernel<D>), grid, dim3(256), 0, st, a);
     if (plan.nsplit > 1)
-      hipLaunchKernelGGL((attn::decode_combine_kernel<bf16, D>), dim3((unsigned)((B * Hq + 3) / 4)), dim3(256), 0,
+      hipLaunchKernelGGL((attn::decode_combine_kernel<bf16, D>), dim3((unsigned)(B * Hq)), dim3(256), 0,
                          st, a.part, O, L, B * Hq, plan.nsplit);
   };
   if (d == 32) launch(std::integral_constant<int, 32>{});

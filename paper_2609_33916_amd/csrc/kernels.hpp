@@ -1117,6 +1117,7 @@ struct DecArgs {
   float* lse;           // [B, Hq] natural log, or null
   int rows;            // B * Hq
   int Hq, Hkv, G, n, n_cap, append;
+  int fuse_append;     // decode_kernel writes the new row itself (one query chunk per cache head)
   int chunk, nsplit, qchunks;
   float sl2;
   uint32_t qflip;
@@ -1185,6 +1186,22 @@ __global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
     ld.issue(stg[2], Vg, kv0, k_hi, w);
     ld.issue(stg[3], Vg, kv0 + 64, k_hi, w);
   };
+  // the workgroup whose split holds row len_b writes the new key and value
+  // there before any of its copies reads the row (no other workgroup reads it)
+  if (a.fuse_append) {
+    const int pos = T_b - 1;
+    if (pos >= k_lo && pos < k_hi) {
+      constexpr int CPR = D / 8;
+      if (tid < 2 * CPR) {
+        const int which = tid / CPR, ch = tid % CPR;
+        const T* src = (const T*)(which ? a.v_new : a.k_new) + (size_t)bh * D + 8 * ch;
+        T* dst = (T*)(which ? a.vc : a.kc) + kvoff + (size_t)pos * D + 8 * ch;
+        *(u32x4*)dst = *(const u32x4*)src;
+        __threadfence();
+      }
+      __syncthreads();
+    }
+  }
   if (nt > 0) issue(stA, k_lo);
   __syncthreads();
 
@@ -1311,38 +1328,54 @@ __global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
 }
 
 // Merge the splits of decode_kernel: per (b, query head), O = sum_s 2^(m_s - M)
-// O_s / sum_s 2^(m_s - M) l_s and L = (M + log2 l) ln 2. One wave per row.
+// O_s / sum_s 2^(m_s - M) l_s and L = (M + log2 l) ln 2. One workgroup per
+// row: thread t takes 4 consecutive d values (t % (D/4)) of the splits
+// s = t / (D/4) + k * SL, and the SL partial sums are added through LDS.
 template <typename T, int D>
 __global__ void __launch_bounds__(256) decode_combine_kernel(const float* part, void* o, float* lse, int rows,
                                                              int nsplit) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (row >= rows) return;
+  constexpr int DL = D / 4, SL = 256 / DL;           // d lanes, split lanes
+  __shared__ float red[256];
+  __shared__ __attribute__((aligned(16))) f32x4 osum[SL][DL];
+  const int row = blockIdx.x, t = threadIdx.x;
   const float* po = part + (size_t)row * nsplit * D;
   const float* pml = part + (size_t)rows * nsplit * D + (size_t)row * nsplit * 2;
-  float M = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, pml[2 * s]);
+  // M = max_s m_s
+  float m = -INFINITY;
+  for (int s = t; s < nsplit; s += 256) m = fmaxf(m, pml[2 * s]);
+  red[t] = m;
+  __syncthreads();
+  for (int k = 128; k > 0; k >>= 1) {
+    if (t < k) red[t] = fmaxf(red[t], red[t + k]);
+    __syncthreads();
+  }
+  const float M = red[0];
+  __syncthreads();
+  const int dl = t % DL, sl = t / DL;
+  f32x4 acc = (f32x4){0.f, 0.f, 0.f, 0.f};
   float l = 0.f;
-  constexpr int DPL = D / 64 > 0 ? D / 64 : 1;       // d values per lane
-  float acc[DPL];
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
+  for (int s = sl; s < nsplit; s += SL) {
     const float f = (M == -INFINITY) ? 0.f : exp2_fast(pml[2 * s] - M);
     l += f * pml[2 * s + 1];
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) {
-      const int dd = lane + 64 * e;
-      if (dd < D) acc[e] += f * po[(size_t)s * D + dd];
-    }
+    const f32x4 v = *(const f32x4*)(po + (size_t)s * D + 4 * dl);
+    acc += f * v;
   }
-  const float inv = l > 0.f ? 1.f / l : 0.f;
-  T* O = (T*)o + (size_t)row * D;
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) {
-    const int dd = lane + 64 * e;
-    if (dd < D) O[dd] = (T)(acc[e] * inv);
+  osum[sl][dl] = acc;
+  red[t] = (dl == 0) ? l : 0.f;
+  __syncthreads();
+  for (int k = 128; k > 0; k >>= 1) {
+    if (t < k) red[t] += red[t + k];
+    __syncthreads();
   }
-  if (lse && lane == 0) lse[row] = l > 0.f ? (M + log2f(l)) * kLn2 : -INFINITY;
+  const float ltot = red[0];
+  if (t < DL) {
+    f32x4 r = osum[0][t];
+#pragma unroll
+    for (int k = 1; k < SL; ++k) r += osum[k][t];
+    const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
+    Quad<T>::store((T*)o + (size_t)row * D + 4 * t, r[0] * inv, r[1] * inv, r[2] * inv, r[3] * inv);
+  }
+  if (lse && t == 0) lse[row] = ltot > 0.f ? (M + log2f(ltot)) * kLn2 : -INFINITY;
 }
 
 // ======================================================================

@@ -65,7 +65,8 @@ def short_name(kernel: str) -> str:
     """Kernel name without template arguments; the backward kernels of the
     materialising path (last template argument MAT = true) get a mat_ prefix."""
     k = kernel.replace("void ", "")
-    for key in ("mat_fwd_kernel", "bwd_prep_kernel", "zero_f32_kernel", "dq_finalize_kernel", "fwd_kernel",
+    for key in ("decode_append_kernel", "decode_combine_kernel", "decode_kernel",
+                "mat_fwd_kernel", "bwd_prep_kernel", "zero_f32_kernel", "dq_finalize_kernel", "fwd_kernel",
                 "dkdv16_kernel", "dkdv_kernel", "dq_kernel", "copyBuffer", "elementwise"):
         if key in k:
             if key == "dkdv16_kernel" and _template_args(k)[-2:] == ["false", "true"]:
