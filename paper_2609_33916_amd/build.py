@@ -42,11 +42,12 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (expected /opt/rocm/bin/hipcc)")
 
 
-def build(verbose: bool = False, out: str = LIB_PATH, extra_flags=()) -> str:
-    """Compile the library (always recompiles) and return its path."""
+def build(verbose: bool = False, out: str = LIB_PATH, extra_flags=(), csrc: str = CSRC) -> str:
+    """Compile the library (always recompiles) and return its path. ``csrc``
+    may name another copy of the sources (variant builds)."""
     tmp = out + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, "-I", CSRC,
-           *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, "-I", csrc,
+           *[os.path.join(csrc, s) for s in SOURCES], "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

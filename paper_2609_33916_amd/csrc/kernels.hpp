@@ -188,13 +188,14 @@ __global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
       // lane (h, c): s[b][j] = raw score of key kv0 + 32b + 16h + j, query qi
       const bool edge = (kv0 + BKV > n) || (CAUSAL && kv0 + BKV - 1 > qw0);
       if (edge) {
+        // keys after `last` are masked; the lane's keys of block b are base_b + j
+        const int last = CAUSAL ? min(qi, n - 1) : n - 1;
 #pragma unroll
-        for (int b = 0; b < NKB; ++b)
+        for (int b = 0; b < NKB; ++b) {
+          const int lim = last - (kv0 + 32 * b + 16 * h);
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int key = kv0 + 32 * b + 16 * h + j;
-            if (key >= n || (CAUSAL && key > qi)) s[b][j] = -INFINITY;
-          }
+          for (int j = 0; j < 16; ++j) s[b][j] = (j > lim) ? -INFINITY : s[b][j];
+        }
       }
       float mx = -INFINITY;
 #pragma unroll
@@ -341,13 +342,13 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
     }
     const bool edge = (kv0 + BKV > n) || (CAUSAL && kv0 + BKV - 1 > qw0);
     if (edge) {
+      const int last = CAUSAL ? min(qi, n - 1) : n - 1;
 #pragma unroll
-      for (int b = 0; b < NKB; ++b)
+      for (int b = 0; b < NKB; ++b) {
+        const int lim = last - (kv0 + 32 * b + 16 * h);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int key = kv0 + 32 * b + 16 * h + j;
-          if (key >= n || (CAUSAL && key > qi)) s[b][j] = -INFINITY;
-        }
+        for (int j = 0; j < 16; ++j) s[b][j] = (j > lim) ? -INFINITY : s[b][j];
+      }
     }
   };
 
@@ -587,6 +588,9 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
       const f32x4* lp = (const f32x4*)&lcur[0][32 * qb + 16 * h];
       const f32x4* dp4 = (const f32x4*)&lcur[1][32 * qb + 16 * h];
       const bool edge = (qb0 + 31 >= n) || (CAUSAL && qb0 < kw0 + 31);
+      // valid queries qb0 + 16h + j: lo <= j <= hi
+      const int qbase = qb0 + 16 * h;
+      const int lo = CAUSAL ? kj - qbase : -1, hi = n - 1 - qbase;
 #pragma unroll
       for (int j4 = 0; j4 < 4; ++j4) {
         const f32x4 l4 = lp[j4], d4 = dp4[j4];
@@ -594,10 +598,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
         for (int e = 0; e < 4; ++e) {
           const int j = 4 * j4 + e;
           float p = MAT ? s[j] : exp2_fast(fmaf(s[j], sl2, -l4[e]));
-          if (edge) {
-            const int q = qb0 + 16 * h + j;
-            if (q >= n || (CAUSAL && kj > q)) p = 0.f;
-          }
+          if (edge) p = (j < lo || j > hi) ? 0.f : p;
           s[j] = p;
           dp[j] = p * (dp[j] - d4[e]);
         }
@@ -767,15 +768,16 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
       const f32x4 d4 = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
       f32x4 l4;
       if constexpr (!MAT) l4 = *(const f32x4*)&lr[0][32 * pb + 16 * x + 4 * g];
+      // valid queries qbase + j: lo <= j <= hi (none for an absent key)
+      const int qbase = qp0 + 16 * x + 4 * g;
+      const int lo = CAUSAL ? kj - qbase : -1;
+      const int hi = ((MAT || AQ) && kj >= n) ? -1 : n - 1 - qbase;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         float p;
         if constexpr (MAT) p = (float)praw[4 * x + j];
         else p = exp2_fast(fmaf(sv[x][j], sl2, -l4[j]));
-        if constexpr (M) {
-          const int q = qp0 + 16 * x + 4 * g + j;
-          if (q >= n || (CAUSAL && kj > q) || ((MAT || AQ) && kj >= n)) p = 0.f;
-        }
+        if constexpr (M) p = (j < lo || j > hi) ? 0.f : p;
         sv[x][j] = p;
         pv[x][j] = p * (pv[x][j] - d4[j]);
       }
@@ -1222,9 +1224,9 @@ __global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
       for (int t = 0; t < TD; ++t) mma(s, RowRead<T, D>::get(kl, kb, t, h, c), qf.f[t]);
       // lane (h, c): s[j] = raw score of key kb0 + 16h + j for query column c
       if (kb0 + 32 > k_hi) {
+        const int lim = k_hi - 1 - (kb0 + 16 * h);
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (kb0 + 16 * h + j >= k_hi) s[j] = -INFINITY;
+        for (int j = 0; j < 16; ++j) s[j] = (j > lim) ? -INFINITY : s[j];
       }
       float mx = -INFINITY;
 #pragma unroll
