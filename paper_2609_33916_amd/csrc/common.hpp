@@ -282,12 +282,12 @@ template <int D> struct RowRead<float, D> {
 
 // Transposed read: A operand = column 32*db + c of the tile, contraction over
 // logical rows of block rb; k-step t covers logical rows 16h + t*KP + [0, KP).
-// The bf16 tiles hold 64 rows. Offsets are reduced modulo the tile size (a
+// The bf16 tiles hold ROWS rows. Offsets are reduced modulo the tile size (a
 // no-op on valid indexes): with the bound visible, the compiler can tell
 // these reads from the LDS DMA into the other stage and does not wait for it.
-template <typename T, int D> struct TransRead;
-template <int D> struct TransRead<bf16, D> {
-  static constexpr int MASK = 64 * D - 1;
+template <typename T, int D, int ROWS = 64> struct TransRead;
+template <int D, int ROWS> struct TransRead<bf16, D, ROWS> {
+  static constexpr int MASK = ROWS * D - 1;
   __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int db, int t, int h, int c) {
     // 16-lane group: source lane q = c % 16 reads stored row base + q/4 and
     // columns [32db + 16*(c/16) + 4*(q%4), +4); the transpose hands lane c
@@ -306,7 +306,7 @@ template <int D> struct TransRead<bf16, D> {
     return __builtin_bit_cast(bf16x8, (u32x4){a[0], a[1], b[0], b[1]});
   }
 };
-template <int D> struct TransRead<float, D> {
+template <int D, int ROWS> struct TransRead<float, D, ROWS> {
   static constexpr int LD = D + Elem<float>::PAD;
   __device__ __forceinline__ static float get(const float* s, int rb, int db, int t, int h, int c) {
     return s[(32 * rb + perm32_inv(16 * h + t)) * LD + 32 * db + c];

@@ -1155,9 +1155,10 @@ __global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
   constexpr int KP = E::KP, TD = D / (2 * KP), T32 = 16 / KP;
   using TL = Tile<T, BKV, D>;
   static_assert(BKV == 64, "TransRead reads 64-row tiles");
-  // two stages, each [K rows 0-63, K rows 64-127, V rows 0-63, V rows 64-127]
-  __shared__ __attribute__((aligned(16))) T stA[4][TL::ELEMS];
-  __shared__ __attribute__((aligned(16))) T stB[4][TL::ELEMS];
+  // V only, two stages of [rows 0-63, rows 64-127]; K goes straight to
+  // registers (the score product reads K rows as they are stored)
+  __shared__ __attribute__((aligned(16))) T st[2][2][TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) float mlw[2][4][32];
 
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, c = lane & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1182,11 +1183,20 @@ __global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
   const int nt = k_hi > k_lo ? (k_hi - k_lo + 127) / 128 : 0;
 
   TileLoader<T, BKV, D> ld(w, lane);
-  auto issue = [&](T (&stg)[4][TL::ELEMS], int kv0) __attribute__((always_inline)) {
-    ld.issue(stg[0], Kg, kv0, k_hi, w);
-    ld.issue(stg[1], Kg, kv0 + 64, k_hi, w);
-    ld.issue(stg[2], Vg, kv0, k_hi, w);
-    ld.issue(stg[3], Vg, kv0 + 64, k_hi, w);
+  // this wave's 32 K rows of a step as A operands: lane c takes key
+  // kv0 + 32w + perm32(c), k-step t its columns 16t + 8h (the layout a row
+  // read of a permuted LDS tile would give); rows past the split repeat its
+  // last row (their scores are masked)
+  auto kload = [&](int kv0, u32x4 (&kr)[TD]) __attribute__((always_inline)) {
+    const int row = min(kv0 + 32 * w + perm32(c), k_hi - 1);
+    const T* src = Kg + (size_t)row * D + 8 * h;
+#pragma unroll
+    for (int t = 0; t < TD; ++t) kr[t] = *(const u32x4*)(src + 16 * t);
+  };
+  auto issue = [&](T (&stg)[2][TL::ELEMS], u32x4 (&kr)[TD], int kv0) __attribute__((always_inline)) {
+    ld.issue(stg[0], Vg, kv0, k_hi, w);
+    ld.issue(stg[1], Vg, kv0 + 64, k_hi, w);
+    kload(kv0, kr);
   };
   // the workgroup whose split holds row len_b writes the new key and value
   // there before any of its copies reads the row (no other workgroup reads it)
@@ -1204,7 +1214,8 @@ __global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
       __syncthreads();
     }
   }
-  if (nt > 0) issue(stA, k_lo);
+  u32x4 kA[TD], kB[TD];
+  if (nt > 0) issue(st[0], kA, k_lo);
   __syncthreads();
 
   f32x16 oacc[NDB];
@@ -1212,16 +1223,16 @@ __global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
   for (int db = 0; db < NDB; ++db) oacc[db] = zero16();
   float m_use = -INFINITY, lsum = 0.f;
 
-  auto step = [&](int it, T (&cur)[4][TL::ELEMS], T (&nxt)[4][TL::ELEMS]) __attribute__((always_inline)) {
+  auto step = [&](int it, T (&cur)[2][TL::ELEMS], u32x4 (&kcur)[TD], T (&nxt)[2][TL::ELEMS],
+                  u32x4 (&knxt)[TD]) __attribute__((always_inline)) {
     const int kv0 = k_lo + it * 128;
-    if (it + 1 < nt) issue(nxt, kv0 + 128);
-    const int kb0 = kv0 + 64 * sub + 32 * kb;        // first key of this wave's block
+    if (it + 1 < nt) issue(nxt, knxt, kv0 + 128);
+    const int kb0 = kv0 + 64 * sub + 32 * kb;        // first key of this wave's block (= kv0 + 32w)
     if (kb0 < k_hi) {
-      const T* kl = cur[sub];
-      const T* vl = cur[2 + sub];
+      const T* vl = cur[sub];
       f32x16 s = zero16();
 #pragma unroll
-      for (int t = 0; t < TD; ++t) mma(s, RowRead<T, D>::get(kl, kb, t, h, c), qf.f[t]);
+      for (int t = 0; t < TD; ++t) mma(s, __builtin_bit_cast(Frag, kcur[t]), qf.f[t]);
       // lane (h, c): s[j] = raw score of key kb0 + 16h + j for query column c
       if (kb0 + 32 > k_hi) {
         const int lim = k_hi - 1 - (kb0 + 16 * h);
@@ -1261,16 +1272,16 @@ __global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
     __syncthreads();
   };
   for (int it = 0; it < nt; it += 2) {
-    step(it, stA, stB);
-    if (it + 1 < nt) step(it + 1, stB, stA);
+    step(it, st[0], kA, st[1], kB);
+    if (it + 1 < nt) step(it + 1, st[1], kB, st[0], kA);
   }
 
   // ---- merge the four waves through LDS (the stage memory is free now):
-  // O parts [4][D][32] in stA, maxima and sums [4][32] each in stB
-  float* ow = (float*)&stA[0][0];
-  float* mw = (float*)&stB[0][0];
-  float* lw = mw + 4 * 32;
-  static_assert(4 * D * 32 * 4 <= 4 * TL::ELEMS * 2, "merge buffer exceeds the stage");
+  // O parts [4][D][32] over both stages, maxima and sums [4][32] each
+  float* ow = (float*)&st[0][0][0];
+  float* mw = &mlw[0][0][0];
+  float* lw = &mlw[1][0][0];
+  static_assert(4 * D * 32 * 4 <= 2 * 2 * TL::ELEMS * 2, "merge buffer exceeds the stages");
   const float ltot = halves_sum(lsum);
   if (h == 0) {
     mw[w * 32 + c] = m_use;
