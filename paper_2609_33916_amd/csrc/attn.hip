@@ -60,19 +60,25 @@ void launch_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
   hipLaunchKernelGGL((attn::fwd_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
 }
 
-// dK/dV: bf16 uses the 16-key-per-wave kernel (8 waves, 128 keys per
-// workgroup, 64-query tiles); float32 the 32-key-per-wave kernel.
+// dK/dV: bf16 uses the 16x16x32 kernel with 128 keys per workgroup and
+// 64-query tiles. For d <= 64 the fused path runs 4 waves of 32 keys (every
+// Q / dO operand read from LDS feeds two products; two waves per SIMD still
+// fit); at d = 128 the 32-key wave needs more than 256 registers, so 8 waves
+// of 16 keys keep two waves per SIMD. The materialising and atomic-dQ forms
+// use 16-key waves. float32 uses the 32-key-per-wave kernel.
 constexpr int kDkv16Waves = 8;
 constexpr int kDkv16BQ = 64;
+constexpr int dkdv_kb(int d, bool mat) { return (mat || d > 64) ? 1 : 2; }
 
 template <typename T, int D, bool CAUSAL, bool MAT = false>
 void launch_dkdv(attn::BwdArgs a, int heads, hipStream_t st) {
   if constexpr (std::is_same<T, bf16>::value) {
-    constexpr int bkv = 16 * kDkv16Waves;
+    constexpr int kb = dkdv_kb(D, MAT), nw = kDkv16Waves / kb;
+    constexpr int bkv = 16 * kb * nw;
     a.ntiles = (a.n + bkv - 1) / bkv;
     a.nblocks = heads * a.ntiles;
-    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, kDkv16Waves, kDkv16BQ, MAT>), dim3(a.nblocks),
-                       dim3(64 * kDkv16Waves), 0, st, a);
+    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, nw, kDkv16BQ, MAT, false, kb>), dim3(a.nblocks),
+                       dim3(64 * nw), 0, st, a);
   } else {
     a.ntiles = (a.n + kDkvBKV - 1) / kDkvBKV;
     a.nblocks = heads * a.ntiles;

@@ -641,10 +641,12 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 
 // ======================================================================
 // dK, dV for bf16 on v_mfma_f32_16x16x32_bf16: a workgroup of NW waves owns
-// 16 * NW keys, 16 per wave (K and V rows of the wave's keys as B operands in
-// registers, dK^T and dV^T accumulators of 16 columns), so a wave needs about
-// half the registers of the 32-key form and two waves share each SIMD: one
-// wave's softmax VALU work overlaps the other's matrix products. Q and dO
+// 16 * KB * NW keys, KB blocks of 16 per wave (K and V rows of the wave's keys
+// as B operands in registers, dK^T and dV^T accumulators of 16 columns per
+// block). Every Q / dO operand read from LDS feeds the KB blocks' products, so
+// KB = 2 halves the LDS reads per product; KB = 1 needs about half the
+// registers, so that at d = 128 two waves still share each SIMD (one wave's
+// softmax VALU work overlaps the other's matrix products). Q and dO
 // tiles of BQ queries (with their base-2 LSE and D rows) are staged in LDS;
 // every 32 queries form one k step of the dV/dK products:
 //   S = Q K^T, dP = dO V^T          (two 16-query blocks each)
@@ -660,10 +662,12 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 // (kept in LDS) for a 16-column slice of d and adds the result to a float32
 // accumulator in HBM with atomic adds (one per element and key block).
 // ======================================================================
-template <int D, bool CAUSAL, int NW, int BQ, bool MAT = false, bool AQ = false>
+template <int D, bool CAUSAL, int NW, int BQ, bool MAT = false, bool AQ = false, int KB = 1>
 __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
-  constexpr int BKV = 16 * NW, NPB = BQ / 32, TD = D / 32, NDB = D / 16;
+  constexpr int KW = 16 * KB;   // keys per wave: KB blocks of 16 share every Q / dO operand read
+  constexpr int BKV = KW * NW, NPB = BQ / 32, TD = D / 32, NDB = D / 16;
   static_assert(!(MAT && AQ), "the materialising backward has its own dQ pass");
+  static_assert(KB == 1 || !(MAT || AQ), "the materialising and atomic-dQ forms use 16-key waves");
   constexpr int PT = MAT ? BQ * BKV : 8;
   constexpr int DST = AQ ? BKV * BQ : 8;   // dS^T tile [BKV keys][BQ queries]
   constexpr int KBL = AQ ? BKV * D : 8;    // the workgroup's K block [BKV][D]
@@ -689,23 +693,26 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   const bf16* dOg = (const bf16*)a.dout + hoff;
   const float* Lg = a.lse2 + (size_t)head * n;
   const float* Dg = a.dvec + (size_t)head * n;
-  const int k0 = kt * BKV, kw0 = k0 + 16 * w, kj = kw0 + c;
+  const int k0 = kt * BKV, kw0 = k0 + KW * w, kj = kw0 + c;
   const bf16* Ag = MAT ? (const bf16*)a.amat + (size_t)head * n * a.lda + k0 : nullptr;
 
-  // B operands: row kj of K (sign-flipped for a negative scale) and of V;
-  // k-step t holds d in [32t + 8g, +8). K is only needed to recompute S.
-  bf16x8 kf[TD], vf[TD];
+  // B operands: row kj + 16 kb of K (sign-flipped for a negative scale) and
+  // of V; k-step t holds d in [32t + 8g, +8). K is only needed to recompute S.
+  bf16x8 kf[KB][TD], vf[KB][TD];
 #pragma unroll
-  for (int t = 0; t < TD; ++t) {
-    u32x4 x = {0u, 0u, 0u, 0u}, y = {0u, 0u, 0u, 0u};
-    if (kj < n) {
-      if (!MAT) x = *(const u32x4*)(Kg + (size_t)kj * D + 32 * t + 8 * g);
-      y = *(const u32x4*)(Vg + (size_t)kj * D + 32 * t + 8 * g);
+  for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+    for (int t = 0; t < TD; ++t) {
+      const int kr = kj + 16 * kb;
+      u32x4 x = {0u, 0u, 0u, 0u}, y = {0u, 0u, 0u, 0u};
+      if (kr < n) {
+        if (!MAT) x = *(const u32x4*)(Kg + (size_t)kr * D + 32 * t + 8 * g);
+        y = *(const u32x4*)(Vg + (size_t)kr * D + 32 * t + 8 * g);
+      }
+      x ^= (u32x4){a.qflip, a.qflip, a.qflip, a.qflip};
+      kf[kb][t] = __builtin_bit_cast(bf16x8, x);
+      vf[kb][t] = __builtin_bit_cast(bf16x8, y);
     }
-    x ^= (u32x4){a.qflip, a.qflip, a.qflip, a.qflip};
-    kf[t] = __builtin_bit_cast(bf16x8, x);
-    vf[t] = __builtin_bit_cast(bf16x8, y);
-  }
 
   const int q_begin = CAUSAL ? (k0 / BQ) * BQ : 0;
   const int nt = (n - q_begin + BQ - 1) / BQ;
@@ -730,35 +737,45 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   }
   __syncthreads();
 
-  f32x4 dk[NDB], dv[NDB];
+  f32x4 dk[KB][NDB], dv[KB][NDB];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db) {
-    dk[db] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    dv[db] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  }
+  for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      dk[kb][db] = (f32x4){0.f, 0.f, 0.f, 0.f};
+      dv[kb][db] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    }
   const float sl2 = a.sl2;
 
   // S (unless MAT) and dP of pair block pb (queries 32pb + [0, 32) of the
   // staged tile)
-  auto sdp = [&](const bf16* ql, const bf16* dol, int pb, f32x4 (&sv)[2], f32x4 (&pv)[2])
+  auto sdp = [&](const bf16* ql, const bf16* dol, int pb, f32x4 (&sv)[KB][2], f32x4 (&pv)[KB][2])
       __attribute__((always_inline)) {
 #pragma unroll
-    for (int x = 0; x < 2; ++x) {
-      sv[x] = (f32x4){0.f, 0.f, 0.f, 0.f};
-      pv[x] = sv[x];
-    }
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        sv[kb][x] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        pv[kb][x] = sv[kb][x];
+      }
 #pragma unroll
     for (int t = 0; t < TD; ++t)
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
-        if (!MAT) mma16(sv[x], row_read16<D>(ql, 2 * pb + x, t, g, c), kf[t]);
-        mma16(pv[x], row_read16<D>(dol, 2 * pb + x, t, g, c), vf[t]);
+        if (!MAT) {
+          const bf16x8 qa = row_read16<D>(ql, 2 * pb + x, t, g, c);
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb) mma16(sv[kb][x], qa, kf[kb][t]);
+        }
+        const bf16x8 oa = row_read16<D>(dol, 2 * pb + x, t, g, c);
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) mma16(pv[kb][x], oa, vf[kb][t]);
       }
   };
   // P = 2^(S sl2 - L) (MAT: P from the staged block), dS = P (dP - D) as
-  // bf16 operands; with MASK, queries >= n, keys >= n and (causal) queries
-  // before key kj get P = 0
-  auto softmax = [&](const float (&lr)[2][BQ], const bf16* pt, int pb, int qp0, f32x4 (&sv)[2],
+  // bf16 operands for the lane's key `key`; with MASK, queries >= n, keys >= n
+  // and (causal) queries before the key get P = 0
+  auto softmax = [&](const float (&lr)[2][BQ], const bf16* pt, int pb, int qp0, int key, f32x4 (&sv)[2],
                      f32x4 (&pv)[2], bf16x8& pf, bf16x8& sf, auto mask) __attribute__((always_inline)) {
     constexpr bool M = decltype(mask)::value;
     bf16x8 praw;
@@ -770,8 +787,8 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
       if constexpr (!MAT) l4 = *(const f32x4*)&lr[0][32 * pb + 16 * x + 4 * g];
       // valid queries qbase + j: lo <= j <= hi (none for an absent key)
       const int qbase = qp0 + 16 * x + 4 * g;
-      const int lo = CAUSAL ? kj - qbase : -1;
-      const int hi = ((MAT || AQ) && kj >= n) ? -1 : n - 1 - qbase;
+      const int lo = CAUSAL ? key - qbase : -1;
+      const int hi = ((MAT || AQ) && key >= n) ? -1 : n - 1 - qbase;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         float p;
@@ -803,8 +820,8 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   float* dQacc = AQ ? a.dqacc + (size_t)head * n * D : nullptr;
   auto dq_products = [&](const bf16* dsT, int qt0p) __attribute__((always_inline)) {
     constexpr int NDT = D / 16, NQT = BQ / 16;
-    constexpr int WPD = NW / NDT, QPW = NQT / WPD;
-    static_assert(NW % NDT == 0 && NQT % WPD == 0, "dQ tiles must split evenly over the waves");
+    constexpr int WPD = AQ ? NW / NDT : 1, QPW = NQT / WPD;
+    static_assert(!AQ || (NW % NDT == 0 && NQT % WPD == 0), "dQ tiles must split evenly over the waves");
     const int dblk = w % NDT, qbase = (w / NDT) * QPW;
     // lane indexes made opaque here so that nothing of this phase is hoisted
     // out of the loop into registers that stay live across the other phases
@@ -826,12 +843,16 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
         if (qrow + 16 * i + j < n) unsafeAtomicAdd(base + (16 * i + j) * D, acc[j]);
     }
   };
-  auto dvdk = [&](const bf16* ql, const bf16* dol, int pb, const bf16x8& pf, const bf16x8& sf)
+  auto dvdk = [&](const bf16* ql, const bf16* dol, int pb, const bf16x8 (&pf)[KB], const bf16x8 (&sf)[KB])
       __attribute__((always_inline)) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      mma16(dv[db], tr_read16<D, BQ>(dol, 32 * pb, db, g, c), pf);
-      mma16(dk[db], tr_read16<D, BQ>(ql, 32 * pb, db, g, c), sf);
+      const bf16x8 oa = tr_read16<D, BQ>(dol, 32 * pb, db, g, c);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) mma16(dv[kb][db], oa, pf[kb]);
+      const bf16x8 qa = tr_read16<D, BQ>(ql, 32 * pb, db, g, c);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) mma16(dk[kb][db], qa, sf[kb]);
     }
   };
 
@@ -861,11 +882,12 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
         if constexpr (AQ) put_ds(dcur, pb, __builtin_bit_cast(bf16x8, (u32x4){0u, 0u, 0u, 0u}));
         continue;
       }
-      f32x4 sv[2], pv[2];
-      bf16x8 pf, sf;
+      f32x4 sv[KB][2], pv[KB][2];
+      bf16x8 pf[KB], sf[KB];
       sdp(cur[0], cur[1], pb, sv, pv);
-      softmax(lcur, pcur, pb, qp0, sv, pv, pf, sf, mask);
-      if constexpr (AQ) put_ds(dcur, pb, sf);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) softmax(lcur, pcur, pb, qp0, kj + 16 * kb, sv[kb], pv[kb], pf[kb], sf[kb], mask);
+      if constexpr (AQ) put_ds(dcur, pb, sf[0]);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
     __syncthreads();
@@ -880,14 +902,17 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
     const int qt0 = q_begin + it * BQ;
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, pnxt);
     dq_prev(it, dprev);
-    f32x4 sv[2][2], pv[2][2];
+    f32x4 sv[2][KB][2], pv[2][KB][2];
     sdp(cur[0], cur[1], 0, sv[0], pv[0]);
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
       if (pb + 1 < NPB) sdp(cur[0], cur[1], pb + 1, sv[(pb + 1) & 1], pv[(pb + 1) & 1]);
-      bf16x8 pf, sf;
-      softmax(lcur, pcur, pb, qt0 + 32 * pb, sv[pb & 1], pv[pb & 1], pf, sf, std::false_type{});
-      if constexpr (AQ) put_ds(dcur, pb, sf);
+      bf16x8 pf[KB], sf[KB];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+        softmax(lcur, pcur, pb, qt0 + 32 * pb, kj + 16 * kb, sv[pb & 1][kb], pv[pb & 1][kb], pf[kb], sf[kb],
+                std::false_type{});
+      if constexpr (AQ) put_ds(dcur, pb, sf[0]);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
     // schedule: S/dP of block 0 with its row reads running ahead; then per
@@ -923,11 +948,11 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
                           (!(MAT || AQ) || k0 + BKV <= n);
     // the pipelined form pays off at d = 128 when S is recomputed; at smaller
     // d a pair block has too few products to hide the exponentials behind
-    if constexpr (D == 128 && !MAT) {
+    if constexpr (D == 128 && !MAT && KB == 1) {
       if (interior) step_inner(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev);
       else step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::true_type{});
     } else {
-      if (interior && MAT) step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::false_type{});
+      if (interior && (MAT || KB > 1)) step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::false_type{});
       else step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::true_type{});
     }
   };
@@ -937,16 +962,20 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
   }
   if constexpr (AQ) dq_products((nt - 1) & 1 ? dsB : dsA, q_begin + (nt - 1) * BQ);
 
-  if (kj < n) {
-    bf16* dKg = (bf16*)a.dk + hoff;
-    bf16* dVg = (bf16*)a.dv + hoff;
-    const float sc = a.dk_scale;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const int col = 16 * db + 4 * g;
-      Quad<bf16>::store(dKg + (size_t)kj * D + col, dk[db][0] * sc, dk[db][1] * sc, dk[db][2] * sc,
-                        dk[db][3] * sc);
-      Quad<bf16>::store(dVg + (size_t)kj * D + col, dv[db][0], dv[db][1], dv[db][2], dv[db][3]);
+  for (int kb = 0; kb < KB; ++kb) {
+    const int kr = kj + 16 * kb;
+    if (kr < n) {
+      bf16* dKg = (bf16*)a.dk + hoff;
+      bf16* dVg = (bf16*)a.dv + hoff;
+      const float sc = a.dk_scale;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const int col = 16 * db + 4 * g;
+        Quad<bf16>::store(dKg + (size_t)kr * D + col, dk[kb][db][0] * sc, dk[kb][db][1] * sc, dk[kb][db][2] * sc,
+                          dk[kb][db][3] * sc);
+        Quad<bf16>::store(dVg + (size_t)kr * D + col, dv[kb][db][0], dv[kb][db][1], dv[kb][db][2], dv[kb][db][3]);
+      }
     }
   }
 }
