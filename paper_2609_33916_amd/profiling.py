@@ -63,15 +63,23 @@ def _last_template_arg_true(kernel: str) -> bool:
 
 def short_name(kernel: str) -> str:
     """Kernel name without template arguments; the backward kernels of the
-    materialising path (last template argument MAT = true) get a mat_ prefix."""
+    materialising path (template argument MAT = true) get a mat_ prefix, the
+    dK/dV kernel of the atomic-dQ form (AQ = true) an atomic_dq_ prefix.
+    dkdv16_kernel<D, CAUSAL, NW, BQ, MAT, AQ, KB>; dkdv_kernel and dq_kernel
+    end in MAT."""
     k = kernel.replace("void ", "")
     for key in ("decode_append_kernel", "decode_combine_kernel", "decode_kernel",
                 "mat_fwd_kernel", "bwd_prep_kernel", "zero_f32_kernel", "dq_finalize_kernel", "fwd_kernel",
                 "dkdv16_kernel", "dkdv_kernel", "dq_kernel", "copyBuffer", "elementwise"):
         if key in k:
-            if key == "dkdv16_kernel" and _template_args(k)[-2:] == ["false", "true"]:
-                return "atomic_dq_" + key
-            if key in ("dkdv16_kernel", "dkdv_kernel", "dq_kernel") and _last_template_arg_true(k):
+            if key == "dkdv16_kernel":
+                args = _template_args(k)
+                if len(args) >= 6 and args[5] == "true":
+                    return "atomic_dq_" + key
+                if len(args) >= 5 and args[4] == "true":
+                    return "mat_" + key
+                return key
+            if key in ("dkdv_kernel", "dq_kernel") and _last_template_arg_true(k):
                 return "mat_" + key
             return key
     return k.split("(")[0][:40]
