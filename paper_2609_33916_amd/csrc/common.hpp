@@ -215,10 +215,28 @@ template <typename T, int ROWS, int D> struct Stage {
   }
 };
 
+// LDS DMA through the buffer path (buffer_load_dword / _dwordx4 ... lds):
+// each lane's `size` bytes at byte offset `off` from the wave-uniform `base`
+// land at lane * size from `lds`. The copies use the buffer form rather than
+// global_load_lds because the latter is a FLAT instruction: while a FLAT
+// copy into LDS is in flight the compiler cannot count LDS reads separately
+// and waits for all of them (lgkmcnt(0)) before the first use, so every
+// operand read of a step that overlaps the next tile's copy would expose its
+// full latency. Offsets stay far below the 2^31-byte range of the resource.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t dma_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, unsigned off, ATTN_LDS void* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, off, 0, 0, 0);
+}
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t r, unsigned off, ATTN_LDS void* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 4, off, 0, 0, 0);
+}
+
 // Global -> LDS transfer of one ROWS x D tile by a 4-wave workgroup.
 // issue() starts the copy of rows [row0, row0 + ROWS) into `lds`; commit()
 // finishes it (the caller's __syncthreads makes it visible).
-//  * bf16: global_load_lds_dwordx4, which writes each lane's 16 bytes at
+//  * bf16: a 16-byte LDS DMA per lane (dma16), which writes each lane's 16 bytes at
 //    lane * 16 of a 1 KB wave-contiguous LDS block; every lane fetches the
 //    global chunk that belongs at its LDS slot (row permutation srow and
 //    chunk swizzle swz applied on the global side), so no registers and no
@@ -245,12 +263,12 @@ template <int ROWS, int D> struct TileLoader<bf16, ROWS, D> {
   }
   __device__ __forceinline__ void issue(bf16* lds, const bf16* g, int row0, int n, int w) const {
     const bool full = row0 + ROWS <= n;
-    const bf16* base = g + (size_t)row0 * D;
+    const auto rs = dma_rsrc(g + (size_t)row0 * D);
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
       int o = off[j];
       if (!full && row0 + xr[j] >= n) o -= (row0 + xr[j] - (n - 1)) * D;
-      __builtin_amdgcn_global_load_lds(base + o, (ATTN_LDS void*)(lds + 512 * (w * NI + j)), 16, 0, 0);
+      dma16(rs, 2u * (unsigned)o, (ATTN_LDS void*)(lds + 512 * (w * NI + j)));
     }
   }
   __device__ __forceinline__ void commit(bf16*) const {}
@@ -360,13 +378,13 @@ template <int ROWS, int D, int NW> struct TileLoader16 {
   }
   __device__ __forceinline__ void issue(bf16* lds, const bf16* g, int row0, int n, int w) const {
     const bool full = row0 + ROWS <= n;
-    const bf16* base = g + (size_t)row0 * D;
+    const auto rs = dma_rsrc(g + (size_t)row0 * D);
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
       if (TI % NW == 0 || w + NW * j < TI) {
         int o = off[j];
         if (!full && row0 + xr[j] >= n) o -= (row0 + xr[j] - (n - 1)) * D;
-        __builtin_amdgcn_global_load_lds(base + o, (ATTN_LDS void*)(lds + 512 * (w + NW * j)), 16, 0, 0);
+        dma16(rs, 2u * (unsigned)o, (ATTN_LDS void*)(lds + 512 * (w + NW * j)));
       }
     }
   }
@@ -396,13 +414,13 @@ template <int ROWS, int COLS, int NW> struct BlockLoader16 {
   }
   __device__ __forceinline__ void issue(bf16* lds, const bf16* g, int row0, int n, int w) const {
     const bool full = row0 + ROWS <= n;
-    const bf16* base = g + (size_t)row0 * ld;
+    const auto rs = dma_rsrc(g + (size_t)row0 * ld);
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
       if (TI % NW == 0 || w + NW * j < TI) {
         int o = off[j];
         if (!full && row0 + xr[j] >= n) o -= (row0 + xr[j] - (n - 1)) * ld;
-        __builtin_amdgcn_global_load_lds(base + o, (ATTN_LDS void*)(lds + 512 * (w + NW * j)), 16, 0, 0);
+        dma16(rs, 2u * (unsigned)o, (ATTN_LDS void*)(lds + 512 * (w + NW * j)));
       }
     }
   }

@@ -544,7 +544,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
     dold.issue(tl[1], dOg, r0, n, w);
     if (w < 2 && (!MAT || w == 1)) {   // MAT reads no L rows
       const int r = min(r0 + lane, n - 1);
-      __builtin_amdgcn_global_load_lds((w == 0 ? Lg : Dg) + r, (ATTN_LDS void*)(ld[w]), 4, 0, 0);
+      dma4(dma_rsrc(w == 0 ? Lg : Dg), 4u * (unsigned)r, (ATTN_LDS void*)(ld[w]));
     }
   };
   auto store_rows = [&](T (&tl)[2][TL::ELEMS]) __attribute__((always_inline)) {
@@ -727,7 +727,7 @@ __global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
     if (w < 2 && (!MAT || w == 1)) {
       const int r = min(r0 + lane, n - 1);
       if (lane < BQ)
-        __builtin_amdgcn_global_load_lds((w == 0 ? Lg : Dg) + r, (ATTN_LDS void*)(lr[w]), 4, 0, 0);
+        dma4(dma_rsrc(w == 0 ? Lg : Dg), 4u * (unsigned)r, (ATTN_LDS void*)(lr[w]));
     }
   };
   load_rows(q_begin, stA, ldA, ptA);
