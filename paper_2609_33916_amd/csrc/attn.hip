@@ -60,20 +60,23 @@ void launch_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
   hipLaunchKernelGGL((attn::fwd_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
 }
 
-// dK/dV: bf16 uses the 16x16x32 kernel with 128 keys per workgroup and
-// 64-query tiles. For d <= 64 the fused path runs 4 waves of 32 keys (every
-// Q / dO operand read from LDS feeds two products; two waves per SIMD still
-// fit); at d = 128 the 32-key wave needs more than 256 registers, so 8 waves
-// of 16 keys keep two waves per SIMD. The materialising and atomic-dQ forms
-// use 16-key waves. float32 uses the 32-key-per-wave kernel.
-constexpr int kDkv16Waves = 8;
+// dK/dV: bf16 uses the 16x16x32 kernel with 64-query tiles. The fused path
+// runs 4-wave workgroups: 32 keys per wave (every Q / dO operand read feeds
+// two products) for d <= 64, 16 keys per wave at d = 128, where a 32-key wave
+// needs more than 256 registers. With 4 waves, the two waves that share a
+// SIMD come from two workgroups whose barriers are independent, so one can
+// run its matrix products while the other waits or runs its softmax. The
+// materialising and atomic-dQ forms use 8 waves of 16 keys (their extra LDS
+// tiles leave room for one workgroup per CU; the atomic form's dQ tiling
+// needs 8 waves). float32 uses the 32-key-per-wave kernel.
 constexpr int kDkv16BQ = 64;
 constexpr int dkdv_kb(int d, bool mat) { return (mat || d > 64) ? 1 : 2; }
+constexpr int dkdv_nw(bool mat) { return mat ? 8 : 4; }
 
 template <typename T, int D, bool CAUSAL, bool MAT = false>
 void launch_dkdv(attn::BwdArgs a, int heads, hipStream_t st) {
   if constexpr (std::is_same<T, bf16>::value) {
-    constexpr int kb = dkdv_kb(D, MAT), nw = kDkv16Waves / kb;
+    constexpr int kb = dkdv_kb(D, MAT), nw = dkdv_nw(MAT);
     constexpr int bkv = 16 * kb * nw;
     a.ntiles = (a.n + bkv - 1) / bkv;
     a.nblocks = heads * a.ntiles;
@@ -97,11 +100,11 @@ void launch_dq(attn::BwdArgs a, int heads, hipStream_t st) {
 template <typename T, int D, bool CAUSAL>
 void launch_dkdv_aq(attn::BwdArgs a, int heads, hipStream_t st) {
   if constexpr (std::is_same<T, bf16>::value) {
-    constexpr int bkv = 16 * kDkv16Waves;
+    constexpr int nw = 8, bkv = 16 * nw;
     a.ntiles = (a.n + bkv - 1) / bkv;
     a.nblocks = heads * a.ntiles;
-    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, kDkv16Waves, kDkv16BQ, false, true>), dim3(a.nblocks),
-                       dim3(64 * kDkv16Waves), 0, st, a);
+    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, nw, kDkv16BQ, false, true>), dim3(a.nblocks),
+                       dim3(64 * nw), 0, st, a);
   }
 }
 

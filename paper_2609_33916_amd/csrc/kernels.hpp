@@ -662,8 +662,10 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 // (kept in LDS) for a 16-column slice of d and adds the result to a float32
 // accumulator in HBM with atomic adds (one per element and key block).
 // ======================================================================
+// (launch bound: at most 256 registers, so that two waves share each SIMD
+// also when a workgroup has fewer than 8 waves)
 template <int D, bool CAUSAL, int NW, int BQ, bool MAT = false, bool AQ = false, int KB = 1>
-__global__ void __launch_bounds__(64 * NW) dkdv16_kernel(const BwdArgs a) {
+__global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   constexpr int KW = 16 * KB;   // keys per wave: KB blocks of 16 share every Q / dO operand read
   constexpr int BKV = KW * NW, NPB = BQ / 32, TD = D / 32, NDB = D / 16;
   static_assert(!(MAT && AQ), "the materialising backward has its own dQ pass");
