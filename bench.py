@@ -89,6 +89,18 @@ def measured_traffic(workload: str, kernel: str):
     return int(k["fetch_bytes"] + k["write_bytes"])
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (first processor in /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
+
+
 def cpu_threads() -> int:
     try:
         from threadpoolctl import threadpool_info
@@ -532,7 +544,8 @@ def main(argv=None) -> int:
             "cores": threads,
             "kind": "oracle",
             "sample": f"{len(heads)} of {B * H} heads (n={n}, d={d}), float64 NumPy naive fwd+bwd "
-                      f"with explicit n x n S and P, {t_cpu:.1f} s",
+                      f"with explicit n x n S and P, {t_cpu:.1f} s on {cpu_model()} ({threads} BLAS "
+                      f"threads); all {B * H} heads extrapolated: {t_cpu / len(heads) * B * H:.0f} s",
         }
     print(json.dumps(record), flush=True)
     return 0
