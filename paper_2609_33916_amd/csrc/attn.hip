@@ -12,13 +12,14 @@
 
 #include "attn_mi355x.h"
 #include "kernels.hpp"
+#include "launch.hpp"
 
 namespace {
 
 using attn::bf16;
 
-constexpr int kFwdBQ = 128;   // queries per forward / dQ workgroup
-constexpr int kDkvBKV = 128;  // keys per dK/dV workgroup
+constexpr int kFwdBQ = attn::kDqBQ;  // queries per forward / dQ workgroup
+constexpr int kDkvBKV = 128;  // keys per float32 dK/dV workgroup
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -60,28 +61,12 @@ void launch_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
   hipLaunchKernelGGL((attn::fwd_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
 }
 
-// dK/dV: bf16 uses the 16x16x32 kernel with 64-query tiles. The fused path
-// runs 4-wave workgroups: 32 keys per wave (every Q / dO operand read feeds
-// two products) for d <= 64, 16 keys per wave at d = 128, where a 32-key wave
-// needs more than 256 registers. With 4 waves, the two waves that share a
-// SIMD come from two workgroups whose barriers are independent, so one can
-// run its matrix products while the other waits or runs its softmax. The
-// materialising and atomic-dQ forms use 8 waves of 16 keys (their extra LDS
-// tiles leave room for one workgroup per CU; the atomic form's dQ tiling
-// needs 8 waves). float32 uses the 32-key-per-wave kernel.
-constexpr int kDkv16BQ = 64;
-constexpr int dkdv_kb(int d, bool mat) { return (mat || d > 64) ? 1 : 2; }
-constexpr int dkdv_nw(bool mat) { return mat ? 8 : 4; }
-
+// bf16 dK/dV and dQ launch from bwd.hip (launch.hpp); float32 uses the
+// 32-key-per-wave dK/dV kernel and the dQ kernel instantiated here.
 template <typename T, int D, bool CAUSAL, bool MAT = false>
 void launch_dkdv(attn::BwdArgs a, int heads, hipStream_t st) {
   if constexpr (std::is_same<T, bf16>::value) {
-    constexpr int kb = dkdv_kb(D, MAT), nw = dkdv_nw(MAT);
-    constexpr int bkv = 16 * kb * nw;
-    a.ntiles = (a.n + bkv - 1) / bkv;
-    a.nblocks = heads * a.ntiles;
-    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, nw, kDkv16BQ, MAT, false, kb>), dim3(a.nblocks),
-                       dim3(64 * nw), 0, st, a);
+    attn::launch_dkdv16<D, CAUSAL, MAT, false>(a, heads, st);
   } else {
     a.ntiles = (a.n + kDkvBKV - 1) / kDkvBKV;
     a.nblocks = heads * a.ntiles;
@@ -91,21 +76,19 @@ void launch_dkdv(attn::BwdArgs a, int heads, hipStream_t st) {
 
 template <typename T, int D, bool CAUSAL, bool MAT = false>
 void launch_dq(attn::BwdArgs a, int heads, hipStream_t st) {
-  a.ntiles = (a.n + kFwdBQ - 1) / kFwdBQ;
-  a.nblocks = heads * a.ntiles;
-  hipLaunchKernelGGL((attn::dq_kernel<T, D, CAUSAL, MAT>), dim3(a.nblocks), dim3(256), 0, st, a);
+  if constexpr (std::is_same<T, bf16>::value) {
+    attn::launch_dq16<D, CAUSAL, MAT>(a, heads, st);
+  } else {
+    a.ntiles = (a.n + kFwdBQ - 1) / kFwdBQ;
+    a.nblocks = heads * a.ntiles;
+    hipLaunchKernelGGL((attn::dq_kernel<T, D, CAUSAL, MAT>), dim3(a.nblocks), dim3(256), 0, st, a);
+  }
 }
 
 // atomic-dQ backward (bfloat16): the dK/dV kernel also accumulates dQ
 template <typename T, int D, bool CAUSAL>
 void launch_dkdv_aq(attn::BwdArgs a, int heads, hipStream_t st) {
-  if constexpr (std::is_same<T, bf16>::value) {
-    constexpr int nw = 8, bkv = 16 * nw;
-    a.ntiles = (a.n + bkv - 1) / bkv;
-    a.nblocks = heads * a.ntiles;
-    hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, nw, kDkv16BQ, false, true>), dim3(a.nblocks),
-                       dim3(64 * nw), 0, st, a);
-  }
+  if constexpr (std::is_same<T, bf16>::value) attn::launch_dkdv16<D, CAUSAL, false, true>(a, heads, st);
 }
 
 template <typename T, int D, bool CAUSAL>

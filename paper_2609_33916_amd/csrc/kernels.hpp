@@ -123,7 +123,7 @@ __global__ void __launch_bounds__(256) bwd_prep_kernel(const PrepArgs a) {
 // queries), online softmax per column, O^T += V^T P^T.
 // ======================================================================
 template <typename T, int D, bool CAUSAL>
-__global__ void __launch_bounds__(256) fwd_kernel(const FwdArgs a) {
+__global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) fwd_kernel(const FwdArgs a) {
   using E = Elem<T>;
   using Frag = typename E::frag;
   constexpr int BQ = 128, BKV = 64, NKB = BKV / 32, NDB = D / 32;
@@ -993,7 +993,7 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
 // the stored matrix (bf16: loaded one key tile ahead into registers).
 // ======================================================================
 template <typename T, int D, bool CAUSAL, bool MAT = false>
-__global__ void __launch_bounds__(256) dq_kernel(const BwdArgs a) {
+__global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) dq_kernel(const BwdArgs a) {
   using E = Elem<T>;
   using Frag = typename E::frag;
   constexpr int BQ = 128, BKV = 64, NKB = BKV / 32, NDB = D / 32;
@@ -1426,7 +1426,7 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(const float* part, 
 // Atomic-dQ support: zero the float32 accumulator, then dQ = scale * acc in
 // the output dtype. HBM-bound, 8 elements per thread.
 // ======================================================================
-__global__ void __launch_bounds__(256) zero_f32_kernel(float* p, long long n8) {
+static __global__ void __launch_bounds__(256) zero_f32_kernel(float* p, long long n8) {
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i < n8) {
     ((f32x4*)p)[2 * i] = (f32x4){0.f, 0.f, 0.f, 0.f};

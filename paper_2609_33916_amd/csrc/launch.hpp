@@ -1,0 +1,34 @@
+// Launchers of the bfloat16 backward kernels (dK/dV on 16x16x32 MFMA, dQ),
+// defined in bwd.hip: a translation unit of its own, compiled with the
+// iterative-ILP machine scheduler (the build script gives each source its
+// flags), while the forward kernels keep the default scheduler.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+
+namespace attn {
+
+// dK/dV tiles: 64 queries per step. The fused path runs 4-wave workgroups:
+// 32 keys per wave (every Q / dO operand read feeds two products) for
+// d <= 64, 16 keys per wave at d = 128, where a 32-key wave needs more than
+// 256 registers. With 4 waves, the two waves that share a SIMD come from two
+// workgroups whose barriers are independent, so one can run its matrix
+// products while the other waits or runs its softmax. The materialising and
+// atomic-dQ forms use 8 waves of 16 keys (their extra LDS tiles leave room
+// for one workgroup per CU; the atomic form's dQ tiling needs 8 waves).
+constexpr int kDkv16BQ = 64;
+constexpr int dkdv16_kb(int d, bool mat_or_aq) { return (mat_or_aq || d > 64) ? 1 : 2; }
+constexpr int dkdv16_nw(bool mat_or_aq) { return mat_or_aq ? 8 : 4; }
+constexpr int dkdv16_bkv(int d, bool mat_or_aq) { return 16 * dkdv16_kb(d, mat_or_aq) * dkdv16_nw(mat_or_aq); }
+// queries per dQ workgroup (as in the forward)
+constexpr int kDqBQ = 128;
+
+// MAT: the backward of the materialising path; AQ: dQ by atomics
+template <int D, bool CAUSAL, bool MAT, bool AQ>
+void launch_dkdv16(BwdArgs a, int heads, hipStream_t st);
+
+template <int D, bool CAUSAL, bool MAT>
+void launch_dq16(BwdArgs a, int heads, hipStream_t st);
+
+}  // namespace attn

@@ -33,8 +33,11 @@ TRAFFIC_TAG = "attn-traffic-json:"
 
 
 def source_hash() -> str:
-    """sha256 over the HIP sources (file names and contents, sorted)."""
+    """sha256 over the HIP sources (file names and contents, sorted) and the
+    compiler flags of each translation unit."""
+    from . import build as _build
     h = hashlib.sha256()
+    h.update(repr((_build.HIPCC_FLAGS, sorted(_build.SOURCES.items()))).encode())
     for fn in sorted(os.listdir(CSRC)):
         if fn.endswith((".hip", ".hpp", ".h")):
             h.update(fn.encode())
