@@ -1,6 +1,7 @@
 // Launches of the bfloat16 backward kernels: dK/dV (dkdv16_kernel) and dQ.
 // Compiled as a separate translation unit with its own scheduler flags; the
-// instantiations below cover every (d, causal, variant) the C ABI dispatches.
+// instantiations below cover every (d, causal, variant) the C ABI dispatches
+// except the atomic-dQ dK/dV kernel, which attn.hip launches itself.
 #include "launch.hpp"
 
 namespace attn {
@@ -24,7 +25,6 @@ void launch_dq16(BwdArgs a, int heads, hipStream_t st) {
 #define ATTN_BWD16_INST(D, C)                                                 \
   template void launch_dkdv16<D, C, false, false>(BwdArgs, int, hipStream_t); \
   template void launch_dkdv16<D, C, true, false>(BwdArgs, int, hipStream_t);  \
-  template void launch_dkdv16<D, C, false, true>(BwdArgs, int, hipStream_t);  \
   template void launch_dq16<D, C, false>(BwdArgs, int, hipStream_t);          \
   template void launch_dq16<D, C, true>(BwdArgs, int, hipStream_t);
 

@@ -24,7 +24,8 @@ constexpr int dkdv16_bkv(int d, bool mat_or_aq) { return 16 * dkdv16_kb(d, mat_o
 // queries per dQ workgroup (as in the forward)
 constexpr int kDqBQ = 128;
 
-// MAT: the backward of the materialising path; AQ: dQ by atomics
+// MAT: the backward of the materialising path; AQ: dQ by atomics (not
+// instantiated in bwd.hip: the atomic-dQ form is launched from attn.hip)
 template <int D, bool CAUSAL, bool MAT, bool AQ>
 void launch_dkdv16(BwdArgs a, int heads, hipStream_t st);
 
