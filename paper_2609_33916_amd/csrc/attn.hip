@@ -91,7 +91,7 @@ void launch_dq(attn::BwdArgs a, int heads, hipStream_t st) {
 template <typename T, int D, bool CAUSAL>
 void launch_dkdv_aq(attn::BwdArgs a, int heads, hipStream_t st) {
   if constexpr (std::is_same<T, bf16>::value) {
-    constexpr int nw = attn::dkdv16_nw(true), bkv = attn::dkdv16_bkv(D, true);
+    constexpr int nw = attn::dkdv16_nw(D, false, true), bkv = attn::dkdv16_bkv(D, false, true);
     a.ntiles = (a.n + bkv - 1) / bkv;
     a.nblocks = heads * a.ntiles;
     hipLaunchKernelGGL((attn::dkdv16_kernel<D, CAUSAL, nw, attn::kDkv16BQ, false, true, 1>), dim3(a.nblocks),

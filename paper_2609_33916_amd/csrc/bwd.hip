@@ -8,11 +8,11 @@ namespace attn {
 
 template <int D, bool CAUSAL, bool MAT, bool AQ>
 void launch_dkdv16(BwdArgs a, int heads, hipStream_t st) {
-  constexpr int kb = dkdv16_kb(D, MAT || AQ), nw = dkdv16_nw(MAT || AQ), bkv = 16 * kb * nw;
+  constexpr int kb = dkdv16_kb(D, MAT || AQ), nw = dkdv16_nw(D, MAT, AQ), bq = dkdv16_bq(D, MAT);
+  constexpr int bkv = 16 * kb * nw;
   a.ntiles = (a.n + bkv - 1) / bkv;
   a.nblocks = heads * a.ntiles;
-  hipLaunchKernelGGL((dkdv16_kernel<D, CAUSAL, nw, kDkv16BQ, MAT, AQ, kb>), dim3(a.nblocks), dim3(64 * nw), 0,
-                     st, a);
+  hipLaunchKernelGGL((dkdv16_kernel<D, CAUSAL, nw, bq, MAT, AQ, kb>), dim3(a.nblocks), dim3(64 * nw), 0, st, a);
 }
 
 template <int D, bool CAUSAL, bool MAT>
