@@ -61,7 +61,9 @@ def _p_checks(P_dev, inp, scale, causal, heads, dtype):
 @pytest.mark.parametrize("d", [32, 64, 128])
 @pytest.mark.parametrize("causal", [False, True])
 def test_naive_ragged_lengths(dtype, d, causal):
-    for n in (1, 2, 63, 65, 129, 1000):
+    # 31/33 straddle the 32-query tiles of the d <= 64 dK/dV kernel, 63/65 the
+    # 64-row tiles, 129 the 128-row ones
+    for n in (1, 2, 31, 33, 63, 65, 129, 1000):
         w = workloads.Workload(f"mat_n{n}_d{d}_{dtype}", 1, 2, n, d, dtype, causal,
                                1.0, 1.0, 1.0 if dtype == "f32" else 0.1, 2000 + n + d)
         inp = workloads.generate(w)
