@@ -1080,6 +1080,17 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) dq_kernel(const B
         if (!MAT) mma(s, RowRead<T, D>::get(kl, kb, t, h, c), qf.f[t]);
         mma(dp, RowRead<T, D>::get(vl, kb, t, h, c), of.f[t]);
       }
+      // without the mask (bf16): keep the K / V row reads two ahead of the
+      // S / dP products (measured 7 % faster at n = 2048, d = 128; under the
+      // mask the same hint measured 5 % slower)
+      if constexpr (!MAT && !CAUSAL && sizeof(T) == 2) {
+        ATTN_SCHED(kSchedDSRead, 2);
+#pragma unroll
+        for (int i = 0; i < 2 * (D / (2 * KP)); ++i) {
+          ATTN_SCHED(kSchedMFMA, 1);
+          ATTN_SCHED(kSchedDSRead, 1);
+        }
+      }
       // lane (h, c): element j is key kb0 + 16h + j, query qi
       const bool edge = (kb0 + 31 >= n) || (CAUSAL && kb0 + 31 > qw0) || (MAT && qw0 + 31 >= n);
 #pragma unroll
