@@ -454,6 +454,93 @@ __device__ __forceinline__ bf16x8 tr_read16(const bf16* s, int r0, int db, int g
   return __builtin_bit_cast(bf16x8, (u32x4){x[0], x[1], y[0], y[1]});
 }
 
+// Padded 16-wide tiles: rows in natural order, chunks in natural order, row
+// stride D + 16 elements (two spare 16-byte chunks). Chunk j of row r sits at
+// bank slot (r (D/8 + 2) + j) mod 16, and (D/8 + 2)/2 is odd for D = 32, 64,
+// 128, so 8 consecutive rows start on 8 distinct even slots: the row read (16
+// rows of one chunk; rows r and r + 8 fall in one pass only with lanes of
+// different parity, which take adjacent chunks) and the transposed read (8
+// rows x 2 adjacent chunks per half-wave) are conflict-free, as with swz16.
+// Unlike the swizzle, a lane's address for k step t or column block db is its
+// own base plus a constant, so the reads of a tile share one address register
+// and differ only in their immediate offsets.
+template <int D> struct Pad16 {
+  static constexpr int RS = D + 16;          // row stride (elements)
+  static constexpr int C = D / 8, CP = C + 2; // data chunks and chunk positions per row
+};
+
+// Global -> LDS DMA of a ROWS x D bf16 tile into the padded layout by NW
+// waves: 1 KB wave instructions over the tile's chunk positions, instruction
+// i issued by wave i % NW. Lanes on a spare chunk take a byte offset beyond
+// the buffer's range, which the buffer unit drops without a memory access
+// (no branch, so the copies stay in the scheduling region of the loop
+// body). Rows >= n fetch row n - 1.
+template <int ROWS, int D, int NW> struct TileLoader16P {
+  static constexpr int CP = Pad16<D>::CP, C = Pad16<D>::C;
+  static constexpr int TI = ROWS * CP / 64;                // wave instructions per tile
+  static constexpr int NI = (TI + NW - 1) / NW;            // per wave (upper bound)
+  static constexpr unsigned kSpare = 0x80000000u;          // out-of-range byte offset
+  static constexpr unsigned kRowBytes = 2u * D;
+  static_assert(ROWS * CP == TI * 64, "tile must split into 1 KB wave blocks");
+  static_assert((D & (D - 1)) == 0, "D must be a power of two");
+  unsigned off[NI];   // byte offset of the lane's chunk in the global rows, kSpare on a spare chunk
+  __device__ __forceinline__ TileLoader16P(int w, int lane) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int P = 64 * (w + NW * j) + lane;   // chunk position in the tile
+      const int s = P / CP, slot = P % CP;
+      off[j] = slot < C ? kRowBytes * s + 16u * slot : kSpare;
+    }
+  }
+  __device__ __forceinline__ void issue(bf16* lds, const bf16* g, int row0, int n, int w) const {
+    const auto rs = dma_rsrc(g + (size_t)row0 * D);
+    if (row0 + ROWS <= n) {
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+        if (TI % NW == 0 || w + NW * j < TI) dma16(rs, off[j], (ATTN_LDS void*)(lds + 512 * (w + NW * j)));
+    } else {
+      const int last = n - 1 - row0;   // last valid row of the tile
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        if (TI % NW == 0 || w + NW * j < TI) {
+          unsigned o = off[j];
+          const int over = (int)(o / kRowBytes) - last;
+          if (o < kSpare && over > 0) o -= (unsigned)over * kRowBytes;
+          dma16(rs, o, (ATTN_LDS void*)(lds + 512 * (w + NW * j)));
+        }
+      }
+    }
+  }
+};
+
+// Row read of a padded tile: A operand = rows 16*rb + c, k-step t covers d in
+// [32t, 32t + 32), lane group g takes d in [32t + 8g, +8). The lane's part of
+// the offset is clamped to its largest value (a no-op) so that alias analysis
+// sees every read stay inside the tile; without that bound the compiler
+// cannot tell the reads from DMA copies in flight into the other stage and
+// waits for those copies first. The rest of the offset is an immediate.
+template <int D>
+__device__ __forceinline__ bf16x8 row_read16p(const bf16* s, int rb, int t, int g, int c) {
+  constexpr int RS = Pad16<D>::RS;
+  const int lp = min(c * RS + 8 * g, 15 * RS + 24);
+  return *(const bf16x8*)(s + lp + 16 * rb * RS + 32 * t);
+}
+
+// Transposed read of a padded tile: A operand = columns 16*db + c, k slots =
+// rows r0 + 4g + [0, 4) and r0 + 16 + 4g + [0, 4); lane (g, c) reads 4
+// elements at column 16*db + 4*(c & 3) of rows r0 + 4g + (c >> 2) and 16
+// rows further (lane part clamped as in row_read16p).
+template <int D>
+__device__ __forceinline__ bf16x8 tr_read16p(const bf16* s, int r0, int db, int g, int c) {
+  constexpr int RS = Pad16<D>::RS;
+  const int lp = min((4 * g + (c >> 2)) * RS + 4 * (c & 3), 15 * RS + 12);
+  const bf16* p0 = s + lp + r0 * RS + 16 * db;
+  i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p0));
+  i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p0 + 16 * RS));
+  const u32x2 x = __builtin_bit_cast(u32x2, lo), y = __builtin_bit_cast(u32x2, hi);
+  return __builtin_bit_cast(bf16x8, (u32x4){x[0], x[1], y[0], y[1]});
+}
+
 // bf16 operand from two 16-row accumulator blocks (slots 0-3 from `a`,
 // 4-7 from `b`).
 __device__ __forceinline__ bf16x8 frag16(const f32x4& a, const f32x4& b) {

@@ -673,8 +673,9 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   constexpr int PT = MAT ? BQ * BKV : 8;
   constexpr int DST = AQ ? BKV * BQ : 8;   // dS^T tile [BKV keys][BQ queries]
   constexpr int KBL = AQ ? BKV * D : 8;    // the workgroup's K block [BKV][D]
-  __shared__ __attribute__((aligned(16))) bf16 stA[2][BQ * D];
-  __shared__ __attribute__((aligned(16))) bf16 stB[2][BQ * D];
+  constexpr int TSZ = BQ * Pad16<D>::RS;  // a padded Q or dO tile (elements)
+  __shared__ __attribute__((aligned(16))) bf16 stA[2][TSZ];
+  __shared__ __attribute__((aligned(16))) bf16 stB[2][TSZ];
   __shared__ __attribute__((aligned(16))) float ldA[2][BQ];
   __shared__ __attribute__((aligned(16))) float ldB[2][BQ];
   __shared__ __attribute__((aligned(16))) bf16 ptA[PT];
@@ -719,9 +720,9 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   const int q_begin = CAUSAL ? (k0 / BQ) * BQ : 0;
   const int nt = (n - q_begin + BQ - 1) / BQ;
 
-  TileLoader16<BQ, D, NW> tld(w, lane);
+  TileLoader16P<BQ, D, NW> tld(w, lane);
   BlockLoader16<BQ, BKV, NW> pld(w, lane, MAT ? (int)a.lda : 0);
-  auto load_rows = [&](int r0, bf16 (&tl)[2][BQ * D], float (&lr)[2][BQ], bf16 (&pt)[PT])
+  auto load_rows = [&](int r0, bf16 (&tl)[2][TSZ], float (&lr)[2][BQ], bf16 (&pt)[PT])
       __attribute__((always_inline)) {
     tld.issue(tl[0], Qg, r0, n, w);
     tld.issue(tl[1], dOg, r0, n, w);
@@ -765,11 +766,11 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
         if (!MAT) {
-          const bf16x8 qa = row_read16<D>(ql, 2 * pb + x, t, g, c);
+          const bf16x8 qa = row_read16p<D>(ql, 2 * pb + x, t, g, c);
 #pragma unroll
           for (int kb = 0; kb < KB; ++kb) mma16(sv[kb][x], qa, kf[kb][t]);
         }
-        const bf16x8 oa = row_read16<D>(dol, 2 * pb + x, t, g, c);
+        const bf16x8 oa = row_read16p<D>(dol, 2 * pb + x, t, g, c);
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) mma16(pv[kb][x], oa, vf[kb][t]);
       }
@@ -849,10 +850,10 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       __attribute__((always_inline)) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      const bf16x8 oa = tr_read16<D, BQ>(dol, 32 * pb, db, g, c);
+      const bf16x8 oa = tr_read16p<D>(dol, 32 * pb, db, g, c);
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) mma16(dv[kb][db], oa, pf[kb]);
-      const bf16x8 qa = tr_read16<D, BQ>(ql, 32 * pb, db, g, c);
+      const bf16x8 qa = tr_read16p<D>(ql, 32 * pb, db, g, c);
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) mma16(dk[kb][db], qa, sf[kb]);
     }
@@ -871,8 +872,8 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   };
   // Pair blocks one after another; with MASK (tiles that touch the diagonal
   // or the end of the sequence) the masks are applied.
-  auto step_seq = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
-                      bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST], auto mask)
+  auto step_seq = [&](int it, bf16 (&cur)[2][TSZ], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
+                      bf16 (&nxt)[2][TSZ], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST], auto mask)
       __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, pnxt);
@@ -898,8 +899,8 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   // valid): software-pipelined, the S/dP products of pair block pb + 1 are
   // issued next to the exponentials of pair block pb, whose dV/dK products
   // follow.
-  auto step_inner = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
-                        bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST])
+  auto step_inner = [&](int it, bf16 (&cur)[2][TSZ], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
+                        bf16 (&nxt)[2][TSZ], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST])
       __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, pnxt);
@@ -919,7 +920,10 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     }
     // schedule: S/dP of block 0 with its row reads running ahead; then per
     // block pb, its exponentials next to the next block's S/dP products and
-    // next to its own dV/dK products (whose transposed reads run ahead)
+    // next to its own dV/dK products (whose transposed reads run ahead). Two
+    // reads per product slot while the next block's S/dP products run: its
+    // row reads and the first transposed reads of block pb, which the padded
+    // tiles leave the registers for.
     ATTN_SCHED(kSchedDSRead, 4);
 #pragma unroll
     for (int i = 0; i < 4 * TD; ++i) { ATTN_SCHED(kSchedMFMA, 1); ATTN_SCHED(kSchedDSRead, 1); }
@@ -929,7 +933,7 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
 #pragma unroll
         for (int i = 0; i < 4 * TD; ++i) {
           ATTN_SCHED(kSchedMFMA, 1);
-          ATTN_SCHED(kSchedDSRead, 1);
+          ATTN_SCHED(kSchedDSRead, 2);
           ATTN_SCHED(kSchedVALU, 2);
         }
       }
@@ -942,8 +946,8 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     }
     __syncthreads();
   };
-  auto step = [&](int it, bf16 (&cur)[2][BQ * D], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
-                  bf16 (&nxt)[2][BQ * D], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST])
+  auto step = [&](int it, bf16 (&cur)[2][TSZ], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
+                  bf16 (&nxt)[2][TSZ], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST])
       __attribute__((always_inline)) {
     const int qt0 = q_begin + it * BQ;
     const bool interior = qt0 + BQ <= n && (!CAUSAL || qt0 >= k0 + BKV - 1) &&
