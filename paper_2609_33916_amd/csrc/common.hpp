@@ -300,28 +300,33 @@ template <int D> struct RowRead<float, D> {
 
 // Transposed read: A operand = column 32*db + c of the tile, contraction over
 // logical rows of block rb; k-step t covers logical rows 16h + t*KP + [0, KP).
-// The bf16 tiles hold ROWS rows. Offsets are reduced modulo the tile size (a
-// no-op on valid indexes): with the bound visible, the compiler can tell
-// these reads from the LDS DMA into the other stage and does not wait for it.
+// The bf16 tiles hold ROWS rows. swz depends only on the low 4 bits of the
+// stored row, which 32*rb + 16*t leave alone, so the lane's offset inside a
+// 16-row group (swizzle included) depends on db and the lane only; rb and t
+// add a constant, which becomes the read's immediate offset. The lane part is
+// clamped to its largest value (a no-op): with the bound visible, the compiler
+// can tell these reads from the LDS DMA into the other stage and does not wait
+// for it.
 template <typename T, int D, int ROWS = 64> struct TransRead;
 template <int D, int ROWS> struct TransRead<bf16, D, ROWS> {
-  static constexpr int MASK = ROWS * D - 1;
-  __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int db, int t, int h, int c) {
+  // offset of lane (h, c) for column block db in the 16 stored rows starting
+  // at a multiple of 16; hi selects the upper 4 logical rows (stored +8)
+  __device__ __forceinline__ static int lane_off(int db, int h, int c, int hi) {
     // 16-lane group: source lane q = c % 16 reads stored row base + q/4 and
     // columns [32db + 16*(c/16) + 4*(q%4), +4); the transpose hands lane c
     // column 32db + c of those 4 rows.
     const int q = c & 15;
-    const int r0 = 32 * rb + 16 * t + 4 * h + (q >> 2);     // logical 16h+8t+k -> stored 16t+4h+k
-    const int r1 = r0 + 8;                                  // logical +4 -> stored +8
+    const int r = 4 * h + (q >> 2) + 8 * hi;                // logical 16h+8t+k -> stored 16t+4h+k
     const int ch = 4 * db + 2 * (c >> 4) + ((q & 3) >> 1);  // 16-byte chunk of the columns
-    const int sub = (q & 1) * 4;
-    const bf16* p0 = s + ((r0 * D + ((ch ^ swz<D>(r0)) * 8) + sub) & MASK);
-    const bf16* p1 = s + ((r1 * D + ((ch ^ swz<D>(r1)) * 8) + sub) & MASK);
-    i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p0));
-    i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(p1));
+    return min(r * D + ((ch ^ swz<D>(r)) * 8) + (q & 1) * 4, 16 * D - 4);
+  }
+  __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int db, int t, int h, int c) {
+    const bf16* b = s + (32 * rb + 16 * t) * D;
+    i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(b + lane_off(db, h, c, 0)));
+    i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(b + lane_off(db, h, c, 1)));
     // whole-register bit casts (element-wise 16-bit inserts are avoided)
-    const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
-    return __builtin_bit_cast(bf16x8, (u32x4){a[0], a[1], b[0], b[1]});
+    const u32x2 a = __builtin_bit_cast(u32x2, lo), e = __builtin_bit_cast(u32x2, hi);
+    return __builtin_bit_cast(bf16x8, (u32x4){a[0], a[1], e[0], e[1]});
   }
 };
 template <int D, int ROWS> struct TransRead<float, D, ROWS> {
