@@ -27,7 +27,9 @@
 // half-wave, and a pass is conflict-free when its lanes touch distinct
 // slots (see swz16 for which lanes share a pass). swz makes the rows of a
 // row read and the 4 rows x 4 chunks of a transposed read land on distinct
-// slots.
+// slots. Two padded forms trade LDS for addresses that are a lane base plus
+// an immediate offset: Pad32 (the forward's K/V tiles at d = 128) and Pad16
+// (the Q/dO tiles of the 16-wide dK/dV kernel).
 // float32 rows are padded by one element instead.
 #pragma once
 
@@ -173,10 +175,30 @@ template <int D> struct RowFrags<float, D> {
 };
 
 // ---------------------------------------------------------- LDS tiles --
-// A ROWS x D tile, row stride LD = D + PAD elements, rows permuted by srow.
-template <typename T, int ROWS, int D> struct Tile {
+// Padded form of the 32-wide bf16 tiles at d = 128 (P = true below): stored
+// rows of 20 16-byte chunk positions (16 data chunks, 4 spare), data chunk j
+// of stored row s at position j ^ key32(s). The bank slot of a chunk is
+// (20 s + (j ^ key32(s))) mod 16 = (4 s + (j ^ key32(s))) mod 16: the row
+// read's 16 lanes of a pass fall into 4 classes of s mod 4 (distinct
+// multiples of 4) and key32 separates the 4 rows of a class; the transposed
+// read's 4 consecutive rows share one key and land on distinct multiples of
+// 4. Both stay conflict-free, as with swz, but the swizzle only touches the
+// two low chunk bits, so a lane's address for k step t or column block db is
+// one of two bases plus an immediate offset instead of one register per t
+// or db. The cost is 25 % more LDS (80 KB for the two K/V stages).
+template <int D> struct Pad32 {
+  static_assert(D == 128, "the padded 32-wide layout is laid out for d = 128");
+  static constexpr int S = D / 8 + 4;   // chunk positions per stored row
+  static constexpr int LD = 8 * S;      // row stride (elements)
+};
+__host__ __device__ constexpr int key32(int s) { return (s >> 2) & 3; }
+
+// A ROWS x D tile, row stride LD = D + PAD elements (P: Pad32<D>::LD), rows
+// permuted by srow.
+template <typename T, int ROWS, int D, bool P = false> struct Tile {
   using E = Elem<T>;
-  static constexpr int LD = D + E::PAD;
+  static_assert(!P || (sizeof(T) == 2 && D == 128), "the padded 32-wide layout is for bf16 at d = 128");
+  static constexpr int LD = P ? 8 * (D / 8 + 4) : D + E::PAD;   // P: Pad32<D>::LD
   static constexpr int ELEMS = ROWS * LD;
   static constexpr int CPR = D / E::CH;            // 16-byte chunks per row
   static constexpr int NCH = ROWS * CPR;
@@ -243,7 +265,7 @@ __device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t r, unsigned off, ATT
 //    LDS write instructions are spent. Rows >= n fetch row n - 1 instead
 //    (finite values; the kernels mask those rows).
 //  * float32: register staging (Stage), rows >= n as zeros.
-template <typename T, int ROWS, int D> struct TileLoader;
+template <typename T, int ROWS, int D, bool P = false> struct TileLoader;
 template <int ROWS, int D> struct TileLoader<bf16, ROWS, D> {
   static constexpr int C = D / 8;                        // 16-byte chunks per row
   static constexpr int NI = ROWS * D * 2 / (4 * 1024);   // wave instructions per tile
@@ -273,6 +295,45 @@ template <int ROWS, int D> struct TileLoader<bf16, ROWS, D> {
   }
   __device__ __forceinline__ void commit(bf16*) const {}
 };
+// bf16, padded layout: 1 KB wave copies over the tile's chunk positions
+// (wave w issues copies w*NI + [0, NI)); lanes on a spare chunk take a byte
+// offset beyond the buffer's range, which the buffer unit drops without a
+// memory access. Rows >= n fetch row n - 1.
+template <int ROWS, int D> struct TileLoader<bf16, ROWS, D, true> {
+  static constexpr int C = D / 8, S = Pad32<D>::S;
+  static constexpr int TI = ROWS * S / 64;          // wave copies per tile
+  static constexpr int NI = TI / 4;                 // per wave (4-wave workgroups)
+  static constexpr unsigned kSpare = 0x80000000u;   // out-of-range byte offset
+  static_assert(NI * 4 * 64 == ROWS * S, "tile must split evenly into 1 KB wave copies");
+  unsigned off[NI];   // byte offset of the lane's chunk in the global rows, kSpare on a spare chunk
+  int xr[NI];         // its logical row
+  __device__ __forceinline__ TileLoader(int w, int lane) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int L = 64 * (w * NI + j) + lane;   // chunk position in the tile
+      const int s = L / S, pos = L % S;
+      const int x = (s & ~31) | perm32(s & 31);
+      xr[j] = x;
+      off[j] = pos < C ? 2u * (unsigned)(x * D + 8 * (pos ^ key32(s))) : kSpare;
+    }
+  }
+  __device__ __forceinline__ void issue(bf16* lds, const bf16* g, int row0, int n, int w) const {
+    const auto rs = dma_rsrc(g + (size_t)row0 * D);
+    if (row0 + ROWS <= n) {
+#pragma unroll
+      for (int j = 0; j < NI; ++j) dma16(rs, off[j], (ATTN_LDS void*)(lds + 512 * (w * NI + j)));
+    } else {
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        unsigned o = off[j];
+        const int over = row0 + xr[j] - (n - 1);
+        if (o != kSpare && over > 0) o -= 2u * (unsigned)(over * D);
+        dma16(rs, o, (ATTN_LDS void*)(lds + 512 * (w * NI + j)));
+      }
+    }
+  }
+  __device__ __forceinline__ void commit(bf16*) const {}
+};
 template <int ROWS, int D> struct TileLoader<float, ROWS, D> {
   Stage<float, ROWS, D> st;
   int tid;
@@ -285,10 +346,20 @@ template <int ROWS, int D> struct TileLoader<float, ROWS, D> {
 
 // Row read: A operand = logical rows of 32-row block `rb` (stored row
 // 32*rb + c), k-step t over d.
-template <typename T, int D> struct RowRead;
+template <typename T, int D, bool P = false> struct RowRead;
 template <int D> struct RowRead<bf16, D> {
   __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int t, int h, int c) {
     return *(const bf16x8*)(s + (32 * rb + c) * D + (((2 * t + h) ^ swz<D>(c)) * 8));
+  }
+};
+// Padded layout: data chunk 2t + h sits at 4 (t >> 1) + ((2 (t & 1) + h) ^
+// key32(c)), so the lane needs one base per parity of t. The lane part is
+// clamped to its largest value (a no-op), as in TransRead.
+template <int D> struct RowRead<bf16, D, true> {
+  static constexpr int LD = Pad32<D>::LD;
+  __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int t, int h, int c) {
+    const int lp = min(c * LD + 8 * ((2 * (t & 1) + h) ^ key32(c)), 31 * LD + 24);
+    return *(const bf16x8*)(s + 32 * rb * LD + 16 * (t & ~1) + lp);
   }
 };
 template <int D> struct RowRead<float, D> {
@@ -307,7 +378,7 @@ template <int D> struct RowRead<float, D> {
 // clamped to its largest value (a no-op): with the bound visible, the compiler
 // can tell these reads from the LDS DMA into the other stage and does not wait
 // for it.
-template <typename T, int D, int ROWS = 64> struct TransRead;
+template <typename T, int D, int ROWS = 64, bool P = false> struct TransRead;
 template <int D, int ROWS> struct TransRead<bf16, D, ROWS> {
   // offset of lane (h, c) for column block db in the 16 stored rows starting
   // at a multiple of 16; hi selects the upper 4 logical rows (stored +8)
@@ -325,6 +396,26 @@ template <int D, int ROWS> struct TransRead<bf16, D, ROWS> {
     i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(b + lane_off(db, h, c, 0)));
     i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(b + lane_off(db, h, c, 1)));
     // whole-register bit casts (element-wise 16-bit inserts are avoided)
+    const u32x2 a = __builtin_bit_cast(u32x2, lo), e = __builtin_bit_cast(u32x2, hi);
+    return __builtin_bit_cast(bf16x8, (u32x4){a[0], a[1], e[0], e[1]});
+  }
+};
+// Padded layout: the 4 rows a lane group reads share one key32, which only
+// permutes the chunks inside an aligned group of 4, so column block db is an
+// immediate offset (32 db) and the lane needs one base per half (rows +0 and
+// +8 of the 16-row group).
+template <int D, int ROWS> struct TransRead<bf16, D, ROWS, true> {
+  static constexpr int LD = Pad32<D>::LD;
+  __device__ __forceinline__ static int lane_off(int h, int c, int hi) {
+    const int q = c & 15;
+    const int r = 4 * h + (q >> 2) + 8 * hi;                // stored row in the 16-row group
+    const int jj = 2 * (c >> 4) + ((q & 3) >> 1);           // chunk inside the aligned group of 4
+    return min(r * LD + 8 * (jj ^ key32(r)) + (q & 1) * 4, 15 * LD + 28);
+  }
+  __device__ __forceinline__ static bf16x8 get(const bf16* s, int rb, int db, int t, int h, int c) {
+    const bf16* b = s + (32 * rb + 16 * t) * LD + 32 * db;
+    i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(b + lane_off(h, c, 0)));
+    i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4*)(b + lane_off(h, c, 1)));
     const u32x2 a = __builtin_bit_cast(u32x2, lo), e = __builtin_bit_cast(u32x2, hi);
     return __builtin_bit_cast(bf16x8, (u32x4){a[0], a[1], e[0], e[1]});
   }

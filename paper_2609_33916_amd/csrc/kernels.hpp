@@ -131,7 +131,9 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) fwd_kernel(const 
   constexpr int KP = E::KP;
   constexpr int TD = D / (2 * KP);   // k-steps over d
   constexpr int T32 = 16 / KP;       // k-steps over a 32-row block
-  using TL = Tile<T, BKV, D>;
+  // bf16 at d = 128: padded K/V tiles (Pad32)
+  static constexpr bool P32 = sizeof(T) == 2 && D == 128;
+  using TL = Tile<T, BKV, D, P32>;
   // two stages of (K, V) in distinct LDS objects: the loop is unrolled by
   // two so every access names its stage statically, which lets the compiler
   // see that reads of one stage never wait on the copy into the other
@@ -155,7 +157,7 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) fwd_kernel(const 
   const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
   const int nt = (kv_end + BKV - 1) / BKV;
 
-  TileLoader<T, BKV, D> kld(w, lane), vld(w, lane);
+  TileLoader<T, BKV, D, P32> kld(w, lane), vld(w, lane);
   kld.issue(stA[0], Kg, 0, n, w);
   vld.issue(stA[1], Vg, 0, n, w);
   kld.commit(stA[0]);
@@ -183,7 +185,7 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) fwd_kernel(const 
       for (int b = 0; b < NKB; ++b) {
         s[b] = zero16();
 #pragma unroll
-        for (int t = 0; t < TD; ++t) mma(s[b], RowRead<T, D>::get(kl, b, t, h, c), qf.f[t]);
+        for (int t = 0; t < TD; ++t) mma(s[b], RowRead<T, D, P32>::get(kl, b, t, h, c), qf.f[t]);
       }
       // lane (h, c): s[b][j] = raw score of key kv0 + 32b + 16h + j, query qi
       const bool edge = (kv0 + BKV > n) || (CAUSAL && kv0 + BKV - 1 > qw0);
@@ -232,7 +234,7 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) fwd_kernel(const 
           const Frag pf = FragFromAcc<T>::get(s[b], t);
 #pragma unroll
           for (int db = 0; db < NDB; ++db)
-            mma(oacc[db], TransRead<T, D>::get(vl, b, db, t, h, c), pf);
+            mma(oacc[db], TransRead<T, D, 64, P32>::get(vl, b, db, t, h, c), pf);
         }
     }
     if (it + 1 < nt) {
@@ -308,7 +310,8 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
   constexpr int KP = E::KP;
   constexpr int TD = D / (2 * KP);
   constexpr int T32 = 16 / KP;
-  using TL = Tile<T, BKV, D>;
+  static constexpr bool P32 = sizeof(T) == 2 && D == 128;   // padded K/V tiles (Pad32)
+  using TL = Tile<T, BKV, D, P32>;
   __shared__ __attribute__((aligned(16))) T stA[2][TL::ELEMS];
   __shared__ __attribute__((aligned(16))) T stB[2][TL::ELEMS];
 
@@ -330,7 +333,7 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
   const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
   const int nt = (kv_end + BKV - 1) / BKV;
   const float sl2 = a.sl2;
-  TileLoader<T, BKV, D> kld(w, lane), vld(w, lane);
+  TileLoader<T, BKV, D, P32> kld(w, lane), vld(w, lane);
 
   // raw scores of key tile kv0 for this lane's query (masked to -inf)
   auto scores = [&](const T* kl, int kv0, f32x16 (&s)[NKB]) __attribute__((always_inline)) {
@@ -338,7 +341,7 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
     for (int b = 0; b < NKB; ++b) {
       s[b] = zero16();
 #pragma unroll
-      for (int t = 0; t < TD; ++t) mma(s[b], RowRead<T, D>::get(kl, b, t, h, c), qf.f[t]);
+      for (int t = 0; t < TD; ++t) mma(s[b], RowRead<T, D, P32>::get(kl, b, t, h, c), qf.f[t]);
     }
     const bool edge = (kv0 + BKV > n) || (CAUSAL && kv0 + BKV - 1 > qw0);
     if (edge) {
@@ -437,7 +440,7 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
           if constexpr (sizeof(T) == 2) pf = __builtin_bit_cast(Frag, pk[b][t]);   // the stored values
           else pf = FragFromAcc<T>::get(s[b], t);
 #pragma unroll
-          for (int db = 0; db < NDB; ++db) mma(oacc[db], TransRead<T, D>::get(cur[1], b, db, t, h, c), pf);
+          for (int db = 0; db < NDB; ++db) mma(oacc[db], TransRead<T, D, 64, P32>::get(cur[1], b, db, t, h, c), pf);
         }
     }
     if (it + 1 < nt) {
@@ -647,7 +650,8 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 // KB = 2 halves the LDS reads per product; KB = 1 needs about half the
 // registers, so that at d = 128 two waves still share each SIMD (one wave's
 // softmax VALU work overlaps the other's matrix products). Q and dO
-// tiles of BQ queries (with their base-2 LSE and D rows) are staged in LDS;
+// tiles of BQ queries (padded rows, Pad16; with their base-2 LSE and D rows)
+// are staged in LDS;
 // every 32 queries form one k step of the dV/dK products:
 //   S = Q K^T, dP = dO V^T          (two 16-query blocks each)
 //   P = 2^(S sl2 - L), dS = P (dP - D)
@@ -1004,7 +1008,10 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) dq_kernel(const B
   static_assert(BKV == 64, "TransRead reads 64-row tiles");
   constexpr int KP = E::KP;
   constexpr int T32 = 16 / KP;
-  using TL = Tile<T, BKV, D>;
+  // swizzled K/V tiles: the padded form (Pad32) frees 20 VGPRs here but measured
+  // about 1 % slower at d = 128
+  static constexpr bool P32 = false;
+  using TL = Tile<T, BKV, D, P32>;
   // two stages of (K, V) in distinct LDS objects (loop unrolled by two)
   __shared__ __attribute__((aligned(16))) T stA[2][TL::ELEMS];
   __shared__ __attribute__((aligned(16))) T stB[2][TL::ELEMS];
@@ -1049,7 +1056,7 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) dq_kernel(const B
   const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
   const int nt = (kv_end + BKV - 1) / BKV;
 
-  TileLoader<T, BKV, D> kld(w, lane), vld(w, lane);
+  TileLoader<T, BKV, D, P32> kld(w, lane), vld(w, lane);
   kld.issue(stA[0], Kg, 0, n, w);
   vld.issue(stA[1], Vg, 0, n, w);
   kld.commit(stA[0]);
@@ -1081,8 +1088,8 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) dq_kernel(const B
       f32x16 s = zero16(), dp = zero16();
 #pragma unroll
       for (int t = 0; t < D / (2 * KP); ++t) {
-        if (!MAT) mma(s, RowRead<T, D>::get(kl, kb, t, h, c), qf.f[t]);
-        mma(dp, RowRead<T, D>::get(vl, kb, t, h, c), of.f[t]);
+        if (!MAT) mma(s, RowRead<T, D, P32>::get(kl, kb, t, h, c), qf.f[t]);
+        mma(dp, RowRead<T, D, P32>::get(vl, kb, t, h, c), of.f[t]);
       }
       // without the mask (bf16): keep the K / V row reads two ahead of the
       // S / dP products (measured 7 % faster at n = 2048, d = 128; under the
@@ -1110,7 +1117,7 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) dq_kernel(const B
       for (int t = 0; t < T32; ++t) {
         const Frag sf = FragFromAcc<T>::get(dp, t);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) mma(dqa[db], TransRead<T, D>::get(kl, kb, db, t, h, c), sf);
+        for (int db = 0; db < NDB; ++db) mma(dqa[db], TransRead<T, D, 64, P32>::get(kl, kb, db, t, h, c), sf);
       }
     }
     if (it + 1 < nt) {
