@@ -925,9 +925,11 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     // schedule: S/dP of block 0 with its row reads running ahead; then per
     // block pb, its exponentials next to the next block's S/dP products and
     // next to its own dV/dK products (whose transposed reads run ahead). Two
-    // reads per product slot while the next block's S/dP products run: its
-    // row reads and the first transposed reads of block pb, which the padded
-    // tiles leave the registers for.
+    // reads and three VALU instructions per product slot while the next
+    // block's S/dP products run: its row reads and the first transposed reads
+    // of block pb (which the padded tiles leave the registers for), and the
+    // exponentials of block pb spread over those products; four VALU
+    // instructions per dV/dK product (the next block's exponentials).
     ATTN_SCHED(kSchedDSRead, 4);
 #pragma unroll
     for (int i = 0; i < 4 * TD; ++i) { ATTN_SCHED(kSchedMFMA, 1); ATTN_SCHED(kSchedDSRead, 1); }
@@ -938,14 +940,14 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
         for (int i = 0; i < 4 * TD; ++i) {
           ATTN_SCHED(kSchedMFMA, 1);
           ATTN_SCHED(kSchedDSRead, 2);
-          ATTN_SCHED(kSchedVALU, 2);
+          ATTN_SCHED(kSchedVALU, 3);
         }
       }
 #pragma unroll
       for (int i = 0; i < 2 * NDB; ++i) {
         ATTN_SCHED(kSchedMFMA, 1);
         ATTN_SCHED(kSchedDSRead, 2);
-        ATTN_SCHED(kSchedVALU, 2);
+        ATTN_SCHED(kSchedVALU, 4);
       }
     }
     __syncthreads();
