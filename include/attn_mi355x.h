@@ -40,6 +40,20 @@
  * on an invalid argument it returns the negative code below and launches
  * nothing. A launch failure reported by the HIP runtime returns ATTN_E_HIP.
  * Faults inside a running kernel surface as errors of later HIP calls.
+ *
+ * Where this interface departs from the plain statement of the problem
+ * (forward, backward and fused forward+backward over B x N x D arrays, Paper
+ * II, section sec:paper2-cpu), on purpose:
+ *  - `dtype` is passed as int (an attn_dtype value) and `stream` as void*
+ *    (a hipStream_t): the same ABI, but the header needs no HIP include and
+ *    foreign-function callers pass plain integers and pointers;
+ *  - the workspace holds two float32 rows per query, not one: the D row and
+ *    the base-2 log-sum-exp row, so the backward kernels read L already in
+ *    the base their exponentials use (attn_workspace_bytes below);
+ *  - ATTN_E_ARG reports a non-finite scale or a causal flag other than 0/1,
+ *    which the other codes do not describe.
+ * The paper defines none of attn_workspace_bytes, attn_strerror or the
+ * status codes: they are part of this interface only.
  */
 #ifndef ATTN_MI355X_H
 #define ATTN_MI355X_H
@@ -69,7 +83,8 @@ enum {
   ATTN_E_ARG = -7          /* scale not finite, or causal not 0/1 */
 };
 
-/* Bytes of device workspace attn_fwd_bwd needs: two float32 per query row,
+/* Not an operation of the paper: the size of the caller-owned scratch rows.
+ * Bytes of device workspace attn_fwd_bwd needs: two float32 per query row,
  * the backward's row pre-pass D_i = sum_j P_ij dP_ij (computed as
  * sum_c dO_ic O_ic) and the row log-sum-exp in base 2 (L_i log2 e), i.e.
  * 2*B*H*n*4 bytes. Returns 0 for non-positive sizes. */
@@ -217,7 +232,8 @@ int attn_decode(const void* q, const void* k_new, const void* v_new, void* k_cac
                 int B, int Hq, int Hkv, int n, int n_cap, int d, float scale, int dtype,
                 void* stream);
 
-/* Static, NUL-terminated description of a status code (never NULL). */
+/* Not an operation of the paper: error reporting of this interface.
+ * Static, NUL-terminated description of a status code (never NULL). */
 const char* attn_strerror(int code);
 
 #ifdef __cplusplus

@@ -109,10 +109,60 @@ def _dtype_code(t: torch.Tensor) -> int:
 def _check(name: str, t: torch.Tensor, ref: torch.Tensor) -> None:
     if not t.is_cuda:
         raise ValueError(f"{name} must be a GPU tensor")
-    if t.dtype != ref.dtype or t.shape != ref.shape or t.device != ref.device:
+    if t.dtype != ref.dtype or tuple(t.shape) != tuple(ref.shape) or t.device != ref.device:
         raise ValueError(f"{name} must match q in dtype, shape and device")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+
+
+def _check_out(name: str, t, shape, dtype: torch.dtype, ref: torch.Tensor) -> None:
+    """An output the kernels write: a contiguous GPU tensor of exactly `shape`
+    and `dtype` on q's device. The C ABI receives only its address, so a
+    wrong size or a host tensor would be written out of bounds."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda or t.device != ref.device:
+        raise ValueError(f"{name} must be a GPU tensor on q's device")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _check_workspace(ws, nbytes: int, ref: torch.Tensor):
+    """A caller-supplied workspace: contiguous, on q's GPU, at least `nbytes`.
+    Returns (pointer, size in bytes)."""
+    if not isinstance(ws, torch.Tensor):
+        raise ValueError("workspace must be a torch.Tensor")
+    if not ws.is_cuda or ws.device != ref.device:
+        raise ValueError("workspace must be a GPU tensor on q's device")
+    if not ws.is_contiguous():
+        raise ValueError("workspace must be contiguous")
+    size = ws.numel() * ws.element_size()
+    if size < nbytes:
+        raise ValueError(f"workspace holds {size} bytes, {nbytes} needed")
+    return ws.data_ptr(), size
+
+
+def _outputs(q: torch.Tensor, out, names):
+    """Preallocated outputs checked against q (each `names` entry is 'x' for a
+    tensor shaped like q, 'L' for the float32 [B, H, n] row vector), or new
+    ones."""
+    B, H, n, _ = q.shape
+    if out is None:
+        return tuple(torch.empty_like(q) if nm != "L" else
+                     torch.empty((B, H, n), dtype=torch.float32, device=q.device) for nm in names)
+    out = tuple(out)
+    if len(out) != len(names):
+        raise ValueError(f"out must hold {len(names)} tensors")
+    for nm, t in zip(names, out):
+        if nm == "L":
+            _check_out("L", t, (B, H, n), torch.float32, q)
+        else:
+            _check_out(nm, t, q.shape, q.dtype, q)
+    return out
 
 
 def _stream(dev: torch.device) -> int:
@@ -131,11 +181,7 @@ def attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: Optional[
     for name, t in (("q", q), ("k", k), ("v", v)):
         _check(name, t, q)
     B, H, n, d = q.shape
-    if out is None:
-        O = torch.empty_like(q)
-        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
-    else:
-        O, L = out
+    O, L = _outputs(q, out, ("O", "L"))
     rc = lib().attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), O.data_ptr(), L.data_ptr(),
                         B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
                         _stream(q.device))
@@ -166,13 +212,14 @@ def attn_bwd(q, k, v, o, lse, do, scale: Optional[float] = None, causal: bool = 
     if lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, n) or not lse.is_contiguous() \
             or lse.device != q.device:
         raise ValueError("lse must be contiguous float32 [B, H, n] on q's device")
-    dQ, dK, dV = (torch.empty_like(q) for _ in range(3)) if out is None else out
+    dQ, dK, dV = _outputs(q, out, ("dQ", "dK", "dV"))
     wsb = attn_workspace_bytes(B, H, n, d)
     if workspace is None:
         workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    ws_ptr, ws_len = _check_workspace(workspace, wsb, q)
     rc = lib().attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
                         do.data_ptr(), dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
-                        workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                        ws_ptr, ws_len,
                         B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
                         _stream(q.device))
     if rc != 0:
@@ -195,18 +242,14 @@ def _fwd_bwd(q, k, v, do, scale, causal, out, workspace, events):
     for name, t in (("q", q), ("k", k), ("v", v), ("do", do)):
         _check(name, t, q)
     B, H, n, d = q.shape
-    if out is None:
-        O = torch.empty_like(q)
-        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
-        dQ, dK, dV = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-    else:
-        O, L, dQ, dK, dV = out
+    O, L, dQ, dK, dV = _outputs(q, out, ("O", "L", "dQ", "dK", "dV"))
     wsb = attn_workspace_bytes(B, H, n, d)
     if workspace is None:
         workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    ws_ptr, ws_len = _check_workspace(workspace, wsb, q)
     args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
             O.data_ptr(), L.data_ptr(), dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
-            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+            ws_ptr, ws_len,
             B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q), _stream(q.device))
     if events is None:
         rc = lib().attn_fwd_bwd(*args)
@@ -235,8 +278,7 @@ def _mat_buffer(q: torch.Tensor, P: Optional[torch.Tensor]) -> torch.Tensor:
     B, H, n, _ = q.shape
     if P is None:
         return torch.empty((B, H, n, attn_mat_lda(n)), dtype=q.dtype, device=q.device)
-    if P.dtype != q.dtype or not P.is_contiguous() or P.device != q.device:
-        raise ValueError("P must be a contiguous tensor of q's dtype on q's device")
+    _check_out("P", P, (B, H, n, attn_mat_lda(n)), q.dtype, q)
     return P
 
 
@@ -248,11 +290,7 @@ def attn_mat_fwd(q, k, v, scale: Optional[float] = None, causal: bool = False, o
     for name, t in (("q", q), ("k", k), ("v", v)):
         _check(name, t, q)
     B, H, n, d = q.shape
-    if out is None:
-        O = torch.empty_like(q)
-        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
-    else:
-        O, L = out
+    O, L = _outputs(q, out, ("O", "L"))
     P = _mat_buffer(q, P)
     rc = lib().attn_mat_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), O.data_ptr(), L.data_ptr(),
                             P.data_ptr(), P.numel() * P.element_size(),
@@ -271,14 +309,18 @@ def attn_mat_bwd(q, k, v, o, do, P, scale: Optional[float] = None, causal: bool 
     for name, t in (("q", q), ("k", k), ("v", v), ("o", o), ("do", do)):
         _check(name, t, q)
     B, H, n, d = q.shape
+    if P is None:
+        raise ValueError("P (the forward's stored attention matrix) is required")
     P = _mat_buffer(q, P)
-    dQ, dK, dV = (torch.empty_like(q) for _ in range(3)) if out is None else out
+    dQ, dK, dV = _outputs(q, out, ("dQ", "dK", "dV"))
+    wsb = attn_workspace_bytes(B, H, n, d)
     if workspace is None:
-        workspace = torch.empty(max(attn_workspace_bytes(B, H, n, d), 1), dtype=torch.uint8, device=q.device)
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    ws_ptr, ws_len = _check_workspace(workspace, wsb, q)
     rc = lib().attn_mat_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), do.data_ptr(),
                             P.data_ptr(), P.numel() * P.element_size(),
                             dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
-                            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                            ws_ptr, ws_len,
                             B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
                             _stream(q.device))
     if rc != 0:
@@ -294,19 +336,16 @@ def attn_mat_fwd_bwd(q, k, v, do, scale: Optional[float] = None, causal: bool = 
     for name, t in (("q", q), ("k", k), ("v", v), ("do", do)):
         _check(name, t, q)
     B, H, n, d = q.shape
-    if out is None:
-        O = torch.empty_like(q)
-        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
-        dQ, dK, dV = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-    else:
-        O, L, dQ, dK, dV = out
+    O, L, dQ, dK, dV = _outputs(q, out, ("O", "L", "dQ", "dK", "dV"))
     P = _mat_buffer(q, P)
+    wsb = attn_workspace_bytes(B, H, n, d)
     if workspace is None:
-        workspace = torch.empty(max(attn_workspace_bytes(B, H, n, d), 1), dtype=torch.uint8, device=q.device)
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    ws_ptr, ws_len = _check_workspace(workspace, wsb, q)
     rc = lib().attn_mat_fwd_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
                                 O.data_ptr(), L.data_ptr(), P.data_ptr(), P.numel() * P.element_size(),
                                 dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
-                                workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                ws_ptr, ws_len,
                                 B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
                                 _stream(q.device))
     if rc != 0:
@@ -328,18 +367,14 @@ def attn_fwd_bwd_atomic(q, k, v, do, scale: Optional[float] = None, causal: bool
     for name, t in (("q", q), ("k", k), ("v", v), ("do", do)):
         _check(name, t, q)
     B, H, n, d = q.shape
-    if out is None:
-        O = torch.empty_like(q)
-        L = torch.empty((B, H, n), dtype=torch.float32, device=q.device)
-        dQ, dK, dV = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-    else:
-        O, L, dQ, dK, dV = out
+    O, L, dQ, dK, dV = _outputs(q, out, ("O", "L", "dQ", "dK", "dV"))
+    wsb = attn_workspace_bytes_atomic(B, H, n, d)
     if workspace is None:
-        workspace = torch.empty(max(attn_workspace_bytes_atomic(B, H, n, d), 16), dtype=torch.uint8,
-                                device=q.device)
+        workspace = torch.empty(max(wsb, 16), dtype=torch.uint8, device=q.device)
+    ws_ptr, ws_len = _check_workspace(workspace, wsb, q)
     rc = lib().attn_fwd_bwd_atomic(q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
                                    O.data_ptr(), L.data_ptr(), dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
-                                   workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                   ws_ptr, ws_len,
                                    B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
                                    _stream(q.device))
     if rc != 0:
@@ -363,18 +398,20 @@ def attn_decode(q, k_cache, v_cache, k_new=None, v_new=None, cache_lens=None, n:
     B, Hq, d = q.shape
     Hkv, n_cap = k_cache.shape[1], k_cache.shape[2]
     for name, t in (("k_cache", k_cache), ("v_cache", v_cache)):
-        if not t.is_cuda or t.dtype != q.dtype or tuple(t.shape) != (B, Hkv, n_cap, d) or not t.is_contiguous():
+        if not t.is_cuda or t.device != q.device or t.dtype != q.dtype or tuple(t.shape) != (B, Hkv, n_cap, d) \
+                or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous GPU tensor [B, Hkv, n_cap, d] of q's dtype")
     if not q.is_cuda or not q.is_contiguous():
         raise ValueError("q must be a contiguous GPU tensor")
     append = k_new is not None
     if append:
         for name, t in (("k_new", k_new), ("v_new", v_new)):
-            if t is None or not t.is_cuda or t.dtype != q.dtype or tuple(t.shape) != (B, Hkv, d) \
-                    or not t.is_contiguous():
+            if t is None or not t.is_cuda or t.device != q.device or t.dtype != q.dtype \
+                    or tuple(t.shape) != (B, Hkv, d) or not t.is_contiguous():
                 raise ValueError(f"{name} must be a contiguous GPU tensor [B, Hkv, d] of q's dtype")
     if cache_lens is not None:
-        if not cache_lens.is_cuda or cache_lens.dtype != torch.int32 or tuple(cache_lens.shape) != (B,):
+        if not cache_lens.is_cuda or cache_lens.device != q.device or cache_lens.dtype != torch.int32 \
+                or tuple(cache_lens.shape) != (B,) or not cache_lens.is_contiguous():
             raise ValueError("cache_lens must be an int32 GPU tensor [B]")
     if n is None:
         if cache_lens is None:
@@ -384,12 +421,19 @@ def attn_decode(q, k_cache, v_cache, k_new=None, v_new=None, cache_lens=None, n:
         O = torch.empty_like(q)
         L = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
     else:
+        if len(out) != 2:
+            raise ValueError("out must hold (O, L)")
         O, L = out
+        _check_out("O", O, (B, Hq, d), q.dtype, q)
+        if L is not None:
+            _check_out("L", L, (B, Hq), torch.float32, q)
     wsb = attn_decode_workspace_bytes(B, Hq, Hkv, n, d, append)
     if workspace is None and wsb > 0:
         workspace = torch.empty(wsb, dtype=torch.uint8, device=q.device)
-    ws_ptr = workspace.data_ptr() if workspace is not None else None
-    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    if workspace is not None:
+        ws_ptr, ws_len = _check_workspace(workspace, wsb, q)
+    else:
+        ws_ptr, ws_len = None, 0
     rc = lib().attn_decode(q.data_ptr(), k_new.data_ptr() if append else None,
                            v_new.data_ptr() if append else None, k_cache.data_ptr(), v_cache.data_ptr(),
                            cache_lens.data_ptr() if cache_lens is not None else None,

@@ -531,9 +531,11 @@ __device__ __forceinline__ bf16x8 row_read16(const bf16* s, int rb, int t, int g
 }
 
 // Transposed read (16-wide): A operand = columns 16*db + c, k slots = rows
-// r0 + 4g + [0, 4) and r0 + 16 + 4g + [0, 4) of a ROWS x D tile. Offsets are
-// reduced modulo the tile size, as in TransRead, so the compiler sees them
-// stay inside the tile.
+// r0 + 4g + [0, 4) and r0 + 16 + 4g + [0, 4) of a ROWS x D tile. Each whole
+// offset is masked with the tile size minus one (a no-op on valid indexes,
+// the tile size being a power of two), so the compiler sees every read stay
+// inside the tile; TransRead and the padded reads instead clamp only the
+// lane's part of the offset.
 template <int D, int ROWS>
 __device__ __forceinline__ bf16x8 tr_read16(const bf16* s, int r0, int db, int g, int c) {
   static_assert((ROWS * D & (ROWS * D - 1)) == 0, "tile size must be a power of two");

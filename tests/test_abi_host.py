@@ -218,3 +218,22 @@ def test_library_source_never_allocates():
         text = open(os.path.join(csrc, fn)).read()
         for call in ("hipMalloc", "hipFree", "hipMallocAsync", "hipExtMalloc", "malloc("):
             assert call not in text, (fn, call)
+
+
+def test_library_imports_no_allocator(L):
+    """The built library links no device or host allocation routine of the
+    HIP runtime, so nothing it runs can obtain an n x n buffer by itself."""
+    import paper_2609_33916_amd as pkg
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-D", "--undefined-only", pkg.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    undefined = [line.split()[-1].split("@")[0] for line in out.splitlines() if line.strip()]
+    assert "hipLaunchKernel" in undefined  # the listing is the library's imports
+    banned = [s for s in undefined
+              if re.match(r"hip(Ext)?(Malloc|Free|MemAlloc|MallocAsync|MallocManaged|HostMalloc|"
+                          r"MallocPitch|Malloc3D|MallocArray|MemPool)", s)]
+    assert banned == [], banned

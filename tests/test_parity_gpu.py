@@ -50,7 +50,7 @@ def test_f32_workloads_every_head(name):
 @pytest.mark.parametrize("name,heads", [
     ("b8h16_n4096_d64_bf16_causal", [(0, 0), (3, 7), (7, 15)]),
     ("b16h32_n2048_d128_bf16_peaked", [(0, 0), (5, 17), (15, 31)]),
-    ("b2h32_n16384_d128_bf16_causal", [(1, 19)]),
+    ("b2h32_n16384_d128_bf16_causal", [(1, 19), (0, 4)]),
 ])
 def test_bf16_workloads_sampled_heads(name, heads):
     """Full-size launch; the oracle recomputes the listed heads in full."""
@@ -155,3 +155,29 @@ def test_backward_entry_point_matches_fused_call():
     for a, b in ((dQ, bQ), (dK, bK), (dV, bV)):
         diff = (a.float() - b.float()).abs().max().item() / a.float().abs().max().item()
         assert diff <= 1e-2, diff
+
+
+def test_longest_workload_sampled_rows_every_head():
+    """n = 16384, d = 128, causal, all 64 heads: O, L and dQ of 48 sampled
+    query rows per head against the oracle restricted to those rows (each
+    depends only on its own row of S and P). The rows include the first, the
+    last and rows next to tile boundaries."""
+    import torch
+    w = workloads.WORKLOADS["b2h32_n16384_d128_bf16_causal"]
+    inp = workloads.generate(w)
+    dev = to_gpu(inp)
+    got = run_fwd_bwd(dev, w.scale, True)
+    n = w.n
+    rng = np.random.default_rng(2024)
+    fixed = np.array([0, 1, 63, 64, 127, 128, 8191, 8192, n - 129, n - 128, n - 2, n - 1])
+    worst = {"O": 0.0, "L": 0.0, "dQ": 0.0}
+    for b in range(w.B):
+        for h in range(w.H):
+            rows = np.unique(np.concatenate([fixed, rng.choice(n, 36, replace=False)]))
+            ref = oracle.rows_forward_dq(inp.q[b, h], inp.k[b, h], inp.v[b, h], inp.do[b, h], rows,
+                                         w.scale, True)
+            idx = torch.from_numpy(rows).to(got["O"].device)
+            for key in worst:
+                x = to_host64(got[key][b, h].index_select(0, idx))
+                worst[key] = max(worst[key], oracle.max_rel_err(x, ref[key]))
+    _check(worst, w.dtype, "n=16384 d=128 causal, 48 rows x 64 heads")
