@@ -80,7 +80,8 @@ enum {
   ATTN_E_WORKSPACE = -5,   /* workspace_bytes < attn_workspace_bytes(B, H, n, d), or
                               p_bytes < attn_mat_bytes(B, H, n, dtype) */
   ATTN_E_HIP = -6,         /* the HIP runtime rejected a kernel launch */
-  ATTN_E_ARG = -7          /* scale not finite, or causal not 0/1 */
+  ATTN_E_ARG = -7,         /* scale not finite, or causal not 0/1 */
+  ATTN_E_SCRATCH = -8      /* attn_fwd_bwd_noalloc: B*H*n > attn_noalloc_max_rows() */
 };
 
 /* Not an operation of the paper: the size of the caller-owned scratch rows.
@@ -104,6 +105,30 @@ int attn_fwd_bwd(const void* Q, const void* K, const void* V, const void* dO,
                  void* workspace, size_t workspace_bytes,
                  int B, int H, int n, int d, float scale, int causal, int dtype,
                  void* stream);
+
+/* ---- Without device allocation -----------------------------------------
+ * For callers that cannot allocate device memory at call time: code being
+ * captured into a HIP graph, tight serving loops, harnesses that forbid
+ * hipMalloc. attn_fwd_bwd_noalloc computes exactly what attn_fwd_bwd computes,
+ * with the same kernels and bit-identical results, but takes no workspace:
+ * the D and base-2 log-sum-exp rows live in a fixed 16 MiB device array of
+ * the library (one per GPU, held from the first call on that GPU until the
+ * process ends), so B*H*n may be at most attn_noalloc_max_rows() = 2097152
+ * query rows (ATTN_E_SCRATCH otherwise; n = 16384 at 64 heads uses half of
+ * it). The call allocates nothing and needs no zeroing: every scratch row is
+ * written by the forward kernel before the backward kernels read it.
+ * All calls on one GPU share that GPU's array and it keeps the last call's
+ * contents: two calls that may run at the same time on one GPU (different
+ * streams, or different host threads without ordering) race on it and give
+ * wrong results; order them on one stream. The first call on a GPU looks the
+ * array's address up (hipGetSymbolAddress) with that GPU current; a failed
+ * lookup returns ATTN_E_HIP. Other arguments and errors as attn_fwd_bwd. */
+size_t attn_noalloc_max_rows(void);
+
+int attn_fwd_bwd_noalloc(const void* Q, const void* K, const void* V, const void* dO,
+                         void* O, float* L, void* dQ, void* dK, void* dV,
+                         int B, int H, int n, int d, float scale, int causal, int dtype,
+                         void* stream);
 
 /* Backward only (Paper II's "Algorithm 1" reads the forward's results back
  * from memory; here only the O(n) row statistics are): dQ, dK, dV from Q, K,

@@ -24,7 +24,8 @@ from typing import Optional, Tuple
 
 import torch  # loads the process's HIP runtime before the library
 
-__all__ = ["attn_fwd", "attn_fwd_bwd", "attn_fwd_bwd_timed", "attn_bwd", "attn_workspace_bytes", "attn_strerror",
+__all__ = ["attn_fwd", "attn_fwd_bwd", "attn_fwd_bwd_timed", "attn_fwd_bwd_noalloc", "attn_noalloc_max_rows",
+           "attn_bwd", "attn_workspace_bytes", "attn_strerror",
            "attn_mat_bytes", "attn_mat_lda", "attn_mat_fwd", "attn_mat_bwd", "attn_mat_fwd_bwd",
            "attn_fwd_bwd_atomic", "attn_workspace_bytes_atomic", "attn_decode", "attn_decode_workspace_bytes",
            "AttnError", "lib", "LIB_PATH", "ATTN_BF16", "ATTN_F32"]
@@ -66,6 +67,10 @@ def lib() -> ctypes.CDLL:
     L.attn_fwd_bwd_timed.restype = i
     L.attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, f, i, i, vp]
     L.attn_bwd.restype = i
+    L.attn_noalloc_max_rows.argtypes = []
+    L.attn_noalloc_max_rows.restype = sz
+    L.attn_fwd_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, f, i, i, vp]
+    L.attn_fwd_bwd_noalloc.restype = i
     L.attn_decode_workspace_bytes.argtypes = [i, i, i, i, i, i]
     L.attn_decode_workspace_bytes.restype = sz
     L.attn_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, i, i, i, i, i, i, f, i, vp]
@@ -199,6 +204,33 @@ def attn_fwd_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, do: torch.Te
     ``out`` may supply preallocated (O, L, dQ, dK, dV) and ``workspace`` a
     uint8 GPU tensor of at least attn_workspace_bytes(B, H, n, d) bytes."""
     return _fwd_bwd(q, k, v, do, scale, causal, out, workspace, None)
+
+
+def attn_noalloc_max_rows() -> int:
+    """Largest B * H * n that attn_fwd_bwd_noalloc accepts."""
+    return int(lib().attn_noalloc_max_rows())
+
+
+def attn_fwd_bwd_noalloc(q, k, v, do, out, scale: Optional[float] = None, causal: bool = False):
+    """attn_fwd_bwd without a workspace: the library's fixed per-GPU scratch
+    holds the D and log-sum-exp rows, so the call allocates nothing. The
+    outputs (O, L, dQ, dK, dV) must be preallocated and passed as ``out``.
+    Calls that may overlap on one GPU race on the shared scratch."""
+    if q.dim() != 4:
+        raise ValueError("q must be [B, H, n, d]")
+    for name, t in (("q", q), ("k", k), ("v", v), ("do", do)):
+        _check(name, t, q)
+    if out is None:
+        raise ValueError("out (O, L, dQ, dK, dV) is required: this entry point allocates nothing")
+    B, H, n, d = q.shape
+    O, L, dQ, dK, dV = _outputs(q, out, ("O", "L", "dQ", "dK", "dV"))
+    rc = lib().attn_fwd_bwd_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
+                                    O.data_ptr(), L.data_ptr(), dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(),
+                                    B, H, n, d, _scale(scale, d), int(bool(causal)), _dtype_code(q),
+                                    _stream(q.device))
+    if rc != 0:
+        raise AttnError(rc, "attn_fwd_bwd_noalloc")
+    return O, L, dQ, dK, dV
 
 
 def attn_bwd(q, k, v, o, lse, do, scale: Optional[float] = None, causal: bool = False,

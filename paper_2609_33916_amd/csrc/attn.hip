@@ -5,9 +5,11 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <limits>
+#include <mutex>
 #include <type_traits>
 
 #include "attn_mi355x.h"
@@ -166,6 +168,37 @@ DecodePlan decode_plan(int B, int Hq, int Hkv, int n, int append) {
   return p;
 }
 
+// Scratch of attn_fwd_bwd_noalloc: the two float32 rows per query (D and
+// the base-2 log-sum-exp) that attn_fwd_bwd keeps in the caller's workspace,
+// in a fixed device array instead. Each GPU holds its own copy from the
+// library's first use on it until the process ends. In host code the name
+// `scratch` is only a stand-in for the symbol: its device address (one per
+// GPU) comes from hipGetSymbolAddress and is the only form passed to kernels.
+constexpr size_t kScratchBytes = size_t(16) << 20;
+static __device__ __align__(256) float scratch[kScratchBytes / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+// Device address of the current GPU's scratch array (looked up once per
+// device, with that device current); nullptr if the lookup failed.
+void* scratch_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+  if (!p) {
+    void* q = nullptr;
+    if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) return nullptr;
+    p = q;
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+
 // Row stride of the materialised attention matrix: n rounded up to a
 // multiple of 128, so every key tile the kernels touch lies inside the row.
 constexpr int kMatMaxN = 1 << 20;
@@ -264,6 +297,23 @@ int attn_fwd_bwd(const void* Q, const void* K, const void* V, const void* dO,
                  int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
   return fwd_bwd_impl(Q, K, V, dO, O, L, dQ, dK, dV, workspace, workspace_bytes,
                       B, H, n, d, scale, causal, dtype, stream, nullptr);
+}
+
+size_t attn_noalloc_max_rows(void) { return kScratchBytes / (2 * sizeof(float)); }
+
+int attn_fwd_bwd_noalloc(const void* Q, const void* K, const void* V, const void* dO,
+                         void* O, float* L, void* dQ, void* dK, void* dV,
+                         int B, int H, int n, int d, float scale, int causal, int dtype, void* stream) {
+  // the same argument checks as attn_fwd_bwd, before the size limit and the
+  // first HIP call
+  if (!Q || !K || !V || !dO || !O || !L || !dQ || !dK || !dV) return ATTN_E_NULL;
+  int rc = check_common(B, H, n, d, scale, causal, dtype);
+  if (rc != ATTN_OK) return rc;
+  if ((long long)B * H * (long long)n > (long long)attn_noalloc_max_rows()) return ATTN_E_SCRATCH;
+  void* ws = scratch_ptr();
+  if (!ws) return ATTN_E_HIP;
+  return fwd_bwd_impl(Q, K, V, dO, O, L, dQ, dK, dV, ws, kScratchBytes, B, H, n, d, scale, causal, dtype,
+                      stream, nullptr);
 }
 
 int attn_bwd(const void* Q, const void* K, const void* V, const void* O, const float* L,
@@ -580,6 +630,8 @@ const char* attn_strerror(int code) {
     case ATTN_E_WORKSPACE: return "workspace smaller than attn_workspace_bytes(), or P smaller than attn_mat_bytes()";
     case ATTN_E_HIP: return "the HIP runtime rejected a kernel launch";
     case ATTN_E_ARG: return "scale is not finite, or causal is not 0 or 1";
+    case ATTN_E_SCRATCH:
+      return "B * H * n exceeds attn_noalloc_max_rows(), the rows the fixed scratch of attn_fwd_bwd_noalloc holds";
     default: return "unknown attn status code";
   }
 }

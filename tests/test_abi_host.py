@@ -41,7 +41,7 @@ def test_workspace_bytes(L):
 
 def test_strerror(L):
     import paper_2609_33916_amd as pkg
-    for code in range(0, -8, -1):
+    for code in range(0, -9, -1):
         s = pkg.attn_strerror(code)
         assert s and "unknown" not in s
     assert "unknown" in pkg.attn_strerror(12345)
@@ -237,3 +237,20 @@ def test_library_imports_no_allocator(L):
               if re.match(r"hip(Ext)?(Malloc|Free|MemAlloc|MallocAsync|MallocManaged|HostMalloc|"
                           r"MallocPitch|Malloc3D|MallocArray|MemPool)", s)]
     assert banned == [], banned
+
+
+def test_noalloc_size_limit_checked_on_the_host(L):
+    """attn_fwd_bwd_noalloc rejects B * H * n beyond its fixed scratch (and
+    the usual bad arguments) before any HIP call."""
+    rows = L.attn_noalloc_max_rows()
+    assert rows == (16 << 20) // 8
+    call = lambda **kw: L.attn_fwd_bwd_noalloc(*(kw.get(k, FAKE) for k in
+                                                 ("Q", "K", "V", "dO", "O", "L", "dQ", "dK", "dV")),
+                                               kw.get("B", 1), kw.get("H", 1), kw.get("n", 8), kw.get("d", 64),
+                                               0.125, 0, 0, None)
+    assert call(n=rows + 1) == -8
+    assert call(B=2, H=2, n=rows // 4 + 1) == -8
+    assert call(Q=None) == -1
+    assert call(dV=None) == -1
+    assert call(d=48) == -3
+    assert call(n=0) == -2
