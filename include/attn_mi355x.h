@@ -87,8 +87,9 @@ enum {
 /* Not an operation of the paper: the size of the caller-owned scratch rows.
  * Bytes of device workspace attn_fwd_bwd needs: two float32 per query row,
  * the backward's row pre-pass D_i = sum_j P_ij dP_ij (computed as
- * sum_c dO_ic O_ic) and the row log-sum-exp in base 2 (L_i log2 e), i.e.
- * 2*B*H*n*4 bytes. Returns 0 for non-positive sizes. */
+ * sum_c dO_ic O_ic and stored negated, the value the backward's dP
+ * accumulators start from) and the row log-sum-exp in base 2 (L_i log2 e),
+ * i.e. 2*B*H*n*4 bytes. Returns 0 for non-positive sizes. */
 size_t attn_workspace_bytes(int B, int H, int n, int d);
 
 /* Forward only: O and L from Q, K, V (Paper I, section sec:paper1, with A

@@ -34,7 +34,7 @@ struct FwdArgs {
   const void* dout;   // optional: when set, D_i = sum_c dO_ic O_ic is written
   void* o;
   float* lse;
-  float* dvec;    // optional: D rows (with dout)
+  float* dvec;    // optional: -D rows (with dout), D_i = sum_c dO_ic O_ic
   float* lse2;    // optional: base-2 log-sum-exp rows, log2 sum_j 2^(S_ij log2 e)
   long long head_stride;  // n * d elements
   int n;
@@ -52,7 +52,7 @@ struct BwdArgs {
   const void* v;
   const void* dout;
   const float* lse2;   // base-2 log-sum-exp rows written by the forward
-  const float* dvec;   // D rows written by the forward
+  const float* dvec;   // -D rows written by the forward (negated D)
   void* dq;
   void* dk;
   void* dv;
@@ -70,7 +70,7 @@ struct BwdArgs {
 };
 
 // ======================================================================
-// Backward pre-pass (attn_bwd): D_i = sum_c dO_ic O_ic and the base-2 log-sum-
+// Backward pre-pass (attn_bwd): -D_i = -sum_c dO_ic O_ic and the base-2 log-sum-
 // exp L_i log2(e) for every row, from a stored O and L. HBM-bound: each row
 // is read once as 16-byte chunks, a group of D/CH lanes per row reduces with
 // cross-lane adds.
@@ -111,7 +111,7 @@ __global__ void __launch_bounds__(256) bwd_prep_kernel(const PrepArgs a) {
 #pragma unroll
   for (int off = G / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
   if (row < a.rows && part == 0) {
-    a.dvec[row] = acc;
+    a.dvec[row] = -acc;   // stored negated: the backward kernels start dP from it
     if (a.lse) a.lse2[row] = a.lse[row] * kLog2e;
   }
 }
@@ -186,6 +186,16 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) fwd_kernel(const 
         s[b] = zero16();
 #pragma unroll
         for (int t = 0; t < TD; ++t) mma(s[b], RowRead<T, D, P32>::get(kl, b, t, h, c), qf.f[t]);
+      }
+      // bf16 at d = 128: K row reads six products ahead of the score products
+      // (measured 1.5-2 % faster forward at n = 16384 than the compiler's two)
+      if constexpr (sizeof(T) == 2 && D == 128) {
+        ATTN_SCHED(kSchedDSRead, 6);
+#pragma unroll
+        for (int i = 0; i < NKB * TD; ++i) {
+          ATTN_SCHED(kSchedMFMA, 1);
+          ATTN_SCHED(kSchedDSRead, 1);
+        }
       }
       // lane (h, c): s[b][j] = raw score of key kv0 + 32b + 16h + j, query qi
       const bool edge = (kv0 + BKV > n) || (CAUSAL && kv0 + BKV - 1 > qw0);
@@ -281,7 +291,7 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) fwd_kernel(const 
     const float l2 = m_use + log2f(ltot);
     a.lse[row] = l2 * kLn2;
     if (dOg) {
-      a.dvec[row] = dsum;
+      a.dvec[row] = -dsum;   // stored negated (the backward starts dP - D from it)
       a.lse2[row] = l2;
     }
   }
@@ -483,7 +493,7 @@ __global__ void __launch_bounds__(256) mat_fwd_kernel(const FwdArgs a) {
     const size_t row = (size_t)head * n + qi;
     a.lse[row] = l2 * kLn2;
     if (dOg) {
-      a.dvec[row] = dsum;
+      a.dvec[row] = -dsum;   // stored negated (the backward starts dP - D from it)
       a.lse2[row] = l2;
     }
   }
@@ -603,7 +613,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
           float p = MAT ? s[j] : exp2_fast(fmaf(s[j], sl2, -l4[e]));
           if (edge) p = (j < lo || j > hi) ? 0.f : p;
           s[j] = p;
-          dp[j] = p * (dp[j] - d4[e]);
+          dp[j] = p * (dp[j] + d4[e]);   // d4 holds -D
         }
       }
 #pragma unroll
@@ -755,16 +765,23 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   const float sl2 = a.sl2;
 
   // S (unless MAT) and dP of pair block pb (queries 32pb + [0, 32) of the
-  // staged tile)
-  auto sdp = [&](const bf16* ql, const bf16* dol, int pb, f32x4 (&sv)[KB][2], f32x4 (&pv)[KB][2])
-      __attribute__((always_inline)) {
+  // staged tile). With FOLD the dP accumulators start from the staged row of
+  // -D (lane group g's queries 4g + [0, 4) of each 16-query block), so the
+  // product leaves dP - D without a subtraction per element; the pipelined
+  // d = 128 step keeps the subtraction in its exponential phase instead (the
+  // earlier -D read there measured 1 % slower against its tuned schedule).
+  auto sdp = [&](const bf16* ql, const bf16* dol, const float (&lr)[2][BQ], int pb, f32x4 (&sv)[KB][2],
+                 f32x4 (&pv)[KB][2], auto fold) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
+    for (int x = 0; x < 2; ++x) {
+      f32x4 init = (f32x4){0.f, 0.f, 0.f, 0.f};
+      if constexpr (decltype(fold)::value) init = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
 #pragma unroll
-      for (int x = 0; x < 2; ++x) {
+      for (int kb = 0; kb < KB; ++kb) {
         sv[kb][x] = (f32x4){0.f, 0.f, 0.f, 0.f};
-        pv[kb][x] = sv[kb][x];
+        pv[kb][x] = init;
       }
+    }
 #pragma unroll
     for (int t = 0; t < TD; ++t)
 #pragma unroll
@@ -780,18 +797,20 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       }
   };
   // P = 2^(S sl2 - L) (MAT: P from the staged block), dS = P (dP - D) as
-  // bf16 operands for the lane's key `key`; with MASK, queries >= n, keys >= n
+  // bf16 operands for the lane's key `key` (with FOLD pv already holds
+  // dP - D, otherwise -D is added here); with MASK, queries >= n, keys >= n
   // and (causal) queries before the key get P = 0
   auto softmax = [&](const float (&lr)[2][BQ], const bf16* pt, int pb, int qp0, int key, f32x4 (&sv)[2],
-                     f32x4 (&pv)[2], bf16x8& pf, bf16x8& sf, auto mask) __attribute__((always_inline)) {
+                     f32x4 (&pv)[2], bf16x8& pf, bf16x8& sf, auto mask, auto fold) __attribute__((always_inline)) {
     constexpr bool M = decltype(mask)::value;
+    constexpr bool F = decltype(fold)::value;
     bf16x8 praw;
     if constexpr (MAT) praw = tr_read16<BKV, BQ>(pt, 32 * pb, w, g, c);
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-      const f32x4 d4 = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
-      f32x4 l4;
+      f32x4 l4, nd4 = (f32x4){0.f, 0.f, 0.f, 0.f};
       if constexpr (!MAT) l4 = *(const f32x4*)&lr[0][32 * pb + 16 * x + 4 * g];
+      if constexpr (!F) nd4 = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
       // valid queries qbase + j: lo <= j <= hi (none for an absent key)
       const int qbase = qp0 + 16 * x + 4 * g;
       const int lo = CAUSAL ? key - qbase : -1;
@@ -803,7 +822,7 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
         else p = exp2_fast(fmaf(sv[x][j], sl2, -l4[j]));
         if constexpr (M) p = (j < lo || j > hi) ? 0.f : p;
         sv[x][j] = p;
-        pv[x][j] = p * (pv[x][j] - d4[j]);
+        pv[x][j] = F ? p * pv[x][j] : p * (pv[x][j] + nd4[j]);
       }
     }
     if constexpr (MAT && !M) pf = praw;
@@ -891,9 +910,10 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       }
       f32x4 sv[KB][2], pv[KB][2];
       bf16x8 pf[KB], sf[KB];
-      sdp(cur[0], cur[1], pb, sv, pv);
+      sdp(cur[0], cur[1], lcur, pb, sv, pv, std::true_type{});
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) softmax(lcur, pcur, pb, qp0, kj + 16 * kb, sv[kb], pv[kb], pf[kb], sf[kb], mask);
+      for (int kb = 0; kb < KB; ++kb)
+        softmax(lcur, pcur, pb, qp0, kj + 16 * kb, sv[kb], pv[kb], pf[kb], sf[kb], mask, std::true_type{});
       if constexpr (AQ) put_ds(dcur, pb, sf[0]);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
@@ -910,15 +930,15 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, pnxt);
     dq_prev(it, dprev);
     f32x4 sv[2][KB][2], pv[2][KB][2];
-    sdp(cur[0], cur[1], 0, sv[0], pv[0]);
+    sdp(cur[0], cur[1], lcur, 0, sv[0], pv[0], std::false_type{});
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
-      if (pb + 1 < NPB) sdp(cur[0], cur[1], pb + 1, sv[(pb + 1) & 1], pv[(pb + 1) & 1]);
+      if (pb + 1 < NPB) sdp(cur[0], cur[1], lcur, pb + 1, sv[(pb + 1) & 1], pv[(pb + 1) & 1], std::false_type{});
       bf16x8 pf[KB], sf[KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
         softmax(lcur, pcur, pb, qt0 + 32 * pb, kj + 16 * kb, sv[pb & 1][kb], pv[pb & 1][kb], pf[kb], sf[kb],
-                std::false_type{});
+                std::false_type{}, std::false_type{});
       if constexpr (AQ) put_ds(dcur, pb, sf[0]);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
@@ -1113,7 +1133,7 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) dq_kernel(const B
           const int key = kb0 + 16 * h + j;
           if (key >= n || (CAUSAL && key > qi) || (MAT && qi >= n)) p = 0.f;
         }
-        dp[j] = p * (dp[j] - dq_);
+        dp[j] = p * (dp[j] + dq_);   // dq_ holds -D
       }
 #pragma unroll
       for (int t = 0; t < T32; ++t) {

@@ -117,3 +117,25 @@ def test_decode_matches_last_row_of_forward():
     a, b = Od.float(), O[:, :, n - 1].float()
     assert (a - b).abs().max().item() <= 1e-2 * b.abs().max().item()
     assert (Ld - L[:, :, n - 1]).abs().max().item() <= 1e-4 * L[:, :, n - 1].abs().max().item()
+
+
+def test_decode_workspace_reused_across_sizes():
+    """One workspace, sized for the largest call, serves calls with different
+    split counts in a row (its contents on entry are ignored); each call
+    meets the oracle."""
+    import torch
+    import paper_2609_33916_amd as lib
+    sizes = [(1, 8, 1, 50000), (3, 16, 4, 2000), (1, 8, 1, 9000), (2, 64, 1, 3000)]
+    cap = max(lib.attn_decode_workspace_bytes(B, Hq, Hkv, n, 128, True) for B, Hq, Hkv, n in sizes)
+    ws = torch.empty(cap, dtype=torch.uint8, device="cuda")
+    for i, (B, Hq, Hkv, n) in enumerate(sizes + sizes[:1]):
+        w = workloads.DecodeWorkload(f"dec_reuse{i}", B, Hq, Hkv, n, n + 1, 128, "bf16", False, 1.0, 700 + i)
+        inp = workloads.generate_decode(w)
+        dev = workloads.decode_to_torch(inp, "cuda")
+        O, L = lib.attn_decode(dev["q"], dev["k_cache"], dev["v_cache"], dev["k_new"], dev["v_new"],
+                               n=n, scale=w.scale, workspace=ws)
+        torch.cuda.synchronize()
+        lens = np.full(B, n, dtype=np.int32)
+        ref = dec.decode_step(inp.q, inp.k_cache, inp.v_cache, lens, w.scale, inp.k_new, inp.v_new)
+        errs = {"O": max_rel(to_host64(O), ref["O"]), "L": max_rel(to_host64(L), ref["L"])}
+        _check(errs, f"reuse {i}: B={B} Hq={Hq} Hkv={Hkv} n={n}")
