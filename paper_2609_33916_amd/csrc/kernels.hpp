@@ -767,9 +767,12 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   // S (unless MAT) and dP of pair block pb (queries 32pb + [0, 32) of the
   // staged tile). With FOLD the dP accumulators start from the staged row of
   // -D (lane group g's queries 4g + [0, 4) of each 16-query block), so the
-  // product leaves dP - D without a subtraction per element; the pipelined
-  // d = 128 step keeps the subtraction in its exponential phase instead (the
-  // earlier -D read there measured 1 % slower against its tuned schedule).
+  // product leaves dP - D without a subtraction per element. That is done at
+  // d <= 64 only: the pipelined d = 128 step keeps the subtraction in its
+  // exponential phase (the earlier -D read there measured 1 % slower against
+  // its tuned schedule), and every step of one d computes dP - D the same
+  // way, so results do not depend on which step form a tile takes.
+  constexpr std::integral_constant<bool, (D <= 64)> kFoldD{};
   auto sdp = [&](const bf16* ql, const bf16* dol, const float (&lr)[2][BQ], int pb, f32x4 (&sv)[KB][2],
                  f32x4 (&pv)[KB][2], auto fold) __attribute__((always_inline)) {
 #pragma unroll
@@ -910,10 +913,10 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       }
       f32x4 sv[KB][2], pv[KB][2];
       bf16x8 pf[KB], sf[KB];
-      sdp(cur[0], cur[1], lcur, pb, sv, pv, std::true_type{});
+      sdp(cur[0], cur[1], lcur, pb, sv, pv, kFoldD);
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
-        softmax(lcur, pcur, pb, qp0, kj + 16 * kb, sv[kb], pv[kb], pf[kb], sf[kb], mask, std::true_type{});
+        softmax(lcur, pcur, pb, qp0, kj + 16 * kb, sv[kb], pv[kb], pf[kb], sf[kb], mask, kFoldD);
       if constexpr (AQ) put_ds(dcur, pb, sf[0]);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
