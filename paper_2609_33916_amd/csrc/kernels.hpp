@@ -655,15 +655,19 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 // ======================================================================
 // dK, dV for bf16 on v_mfma_f32_16x16x32_bf16: a workgroup of NW waves owns
 // 16 * KB * NW keys, KB blocks of 16 per wave (K and V rows of the wave's keys
-// as B operands in registers, dK^T and dV^T accumulators of 16 columns per
-// block). Every Q / dO operand read from LDS feeds the KB blocks' products, so
-// KB = 2 halves the LDS reads per product; KB = 1 needs about half the
-// registers, so that at d = 128 two waves still share each SIMD (one wave's
-// softmax VALU work overlaps the other's matrix products). Q and dO
-// tiles of BQ queries (padded rows, Pad16; with their base-2 LSE and D rows)
-// are staged in LDS;
+// as B operands, dK^T and dV^T accumulators of 16 columns per block). Every
+// Q / dO operand read from LDS feeds the KB blocks' products, so KB = 2
+// halves the LDS bytes per product. V is held in registers; K too, except at
+// d = 128 with KB = 2 (KL), where the K operands are read from an LDS copy of
+// the workgroup's key block, staged once: in registers they would take 32 of
+// the VGPRs that two waves per SIMD leave (one wave's softmax VALU work
+// overlaps the other's matrix products). KL still reads 0.625x the LDS bytes
+// per product of 16-key waves. KB = 1 serves the materialising and atomic-dQ
+// forms. Q and dO tiles of BQ queries (padded rows, Pad16; with their base-2
+// LSE and -D rows) are staged in LDS;
 // every 32 queries form one k step of the dV/dK products:
-//   S = Q K^T, dP = dO V^T          (two 16-query blocks each)
+//   S = Q K^T, dP - D = dO V^T - D   (two 16-query blocks each; the dP
+//                                     accumulators start from -D)
 //   P = 2^(S sl2 - L), dS = P (dP - D)
 //   dV^T += dO^T P, dK^T += Q^T dS  (contraction over the 32 queries)
 // With MAT (the backward of the materialising path) S and the exponentials
@@ -697,6 +701,9 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 dsA[DST];
   __shared__ __attribute__((aligned(16))) bf16 dsB[DST];
   __shared__ __attribute__((aligned(16))) bf16 kbl[KBL];
+  constexpr bool KL = KB > 1 && D > 64;
+  static_assert(!KL || BQ == 32, "the KL step takes one pair block of queries");
+  __shared__ __attribute__((aligned(16))) bf16 kst[KL ? BKV * Pad16<D>::RS : 8];
 
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -713,8 +720,9 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   const int k0 = kt * BKV, kw0 = k0 + KW * w, kj = kw0 + c;
   const bf16* Ag = MAT ? (const bf16*)a.amat + (size_t)head * n * a.lda + k0 : nullptr;
 
-  // B operands: row kj + 16 kb of K (sign-flipped for a negative scale) and
-  // of V; k-step t holds d in [32t + 8g, +8). K is only needed to recompute S.
+  // B operands: row kj + 16 kb of K (sign-flipped for a negative scale; with
+  // KL read from LDS instead) and of V; k-step t holds d in [32t + 8g, +8). K
+  // is only needed to recompute S.
   bf16x8 kf[KB][TD], vf[KB][TD];
 #pragma unroll
   for (int kb = 0; kb < KB; ++kb)
@@ -723,7 +731,7 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       const int kr = kj + 16 * kb;
       u32x4 x = {0u, 0u, 0u, 0u}, y = {0u, 0u, 0u, 0u};
       if (kr < n) {
-        if (!MAT) x = *(const u32x4*)(Kg + (size_t)kr * D + 32 * t + 8 * g);
+        if (!MAT && !KL) x = *(const u32x4*)(Kg + (size_t)kr * D + 32 * t + 8 * g);
         y = *(const u32x4*)(Vg + (size_t)kr * D + 32 * t + 8 * g);
       }
       x ^= (u32x4){a.qflip, a.qflip, a.qflip, a.qflip};
@@ -752,6 +760,10 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     TileLoader16<BKV, D, NW> kbld(w, lane);
     kbld.issue(kbl, Kg, k0, n, w);
   }
+  if constexpr (KL) {
+    TileLoader16P<BKV, D, NW> kld(w, lane);
+    kld.issue(kst, Kg, k0, n, w);
+  }
   __syncthreads();
 
   f32x4 dk[KB][NDB], dv[KB][NDB];
@@ -762,23 +774,21 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       dk[kb][db] = (f32x4){0.f, 0.f, 0.f, 0.f};
       dv[kb][db] = (f32x4){0.f, 0.f, 0.f, 0.f};
     }
-  const float sl2 = a.sl2;
+  // KL: a negative scale enters as the sign of sl2 instead of a sign flip of
+  // K (the same products with the same signs)
+  const float sl2 = (KL && a.qflip) ? -a.sl2 : a.sl2;
 
-  // S (unless MAT) and dP of pair block pb (queries 32pb + [0, 32) of the
-  // staged tile). With FOLD the dP accumulators start from the staged row of
-  // -D (lane group g's queries 4g + [0, 4) of each 16-query block), so the
-  // product leaves dP - D without a subtraction per element. That is done at
-  // d <= 64 only: the pipelined d = 128 step keeps the subtraction in its
-  // exponential phase (the earlier -D read there measured 1 % slower against
-  // its tuned schedule), and every step of one d computes dP - D the same
-  // way, so results do not depend on which step form a tile takes.
-  constexpr std::integral_constant<bool, (D <= 64)> kFoldD{};
+  // S (unless MAT) and dP - D of pair block pb (queries 32pb + [0, 32) of
+  // the staged tile): the dP accumulators start from the staged row of -D
+  // (lane group g's queries 4g + [0, 4) of each 16-query block), so the
+  // product leaves dP - D without a subtraction per element. Every step form
+  // does this the same way, so results do not depend on which form a tile
+  // takes (and the atomic-dQ form's dK and dV equal the fused path's).
   auto sdp = [&](const bf16* ql, const bf16* dol, const float (&lr)[2][BQ], int pb, f32x4 (&sv)[KB][2],
-                 f32x4 (&pv)[KB][2], auto fold) __attribute__((always_inline)) {
+                 f32x4 (&pv)[KB][2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-      f32x4 init = (f32x4){0.f, 0.f, 0.f, 0.f};
-      if constexpr (decltype(fold)::value) init = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
+      const f32x4 init = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
         sv[kb][x] = (f32x4){0.f, 0.f, 0.f, 0.f};
@@ -786,34 +796,35 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       }
     }
 #pragma unroll
-    for (int t = 0; t < TD; ++t)
+    for (int t = 0; t < TD; ++t) {
+      bf16x8 kop[KB];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) kop[kb] = KL ? row_read16p<D>(kst, KB * w + kb, t, g, c) : kf[kb][t];
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
         if (!MAT) {
           const bf16x8 qa = row_read16p<D>(ql, 2 * pb + x, t, g, c);
 #pragma unroll
-          for (int kb = 0; kb < KB; ++kb) mma16(sv[kb][x], qa, kf[kb][t]);
+          for (int kb = 0; kb < KB; ++kb) mma16(sv[kb][x], qa, kop[kb]);
         }
         const bf16x8 oa = row_read16p<D>(dol, 2 * pb + x, t, g, c);
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) mma16(pv[kb][x], oa, vf[kb][t]);
       }
+    }
   };
   // P = 2^(S sl2 - L) (MAT: P from the staged block), dS = P (dP - D) as
-  // bf16 operands for the lane's key `key` (with FOLD pv already holds
-  // dP - D, otherwise -D is added here); with MASK, queries >= n, keys >= n
-  // and (causal) queries before the key get P = 0
+  // bf16 operands for the lane's key `key` (pv holds dP - D); with MASK,
+  // queries >= n, keys >= n and (causal) queries before the key get P = 0
   auto softmax = [&](const float (&lr)[2][BQ], const bf16* pt, int pb, int qp0, int key, f32x4 (&sv)[2],
-                     f32x4 (&pv)[2], bf16x8& pf, bf16x8& sf, auto mask, auto fold) __attribute__((always_inline)) {
+                     f32x4 (&pv)[2], bf16x8& pf, bf16x8& sf, auto mask) __attribute__((always_inline)) {
     constexpr bool M = decltype(mask)::value;
-    constexpr bool F = decltype(fold)::value;
     bf16x8 praw;
     if constexpr (MAT) praw = tr_read16<BKV, BQ>(pt, 32 * pb, w, g, c);
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-      f32x4 l4, nd4 = (f32x4){0.f, 0.f, 0.f, 0.f};
+      f32x4 l4;
       if constexpr (!MAT) l4 = *(const f32x4*)&lr[0][32 * pb + 16 * x + 4 * g];
-      if constexpr (!F) nd4 = *(const f32x4*)&lr[1][32 * pb + 16 * x + 4 * g];
       // valid queries qbase + j: lo <= j <= hi (none for an absent key)
       const int qbase = qp0 + 16 * x + 4 * g;
       const int lo = CAUSAL ? key - qbase : -1;
@@ -825,7 +836,7 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
         else p = exp2_fast(fmaf(sv[x][j], sl2, -l4[j]));
         if constexpr (M) p = (j < lo || j > hi) ? 0.f : p;
         sv[x][j] = p;
-        pv[x][j] = F ? p * pv[x][j] : p * (pv[x][j] + nd4[j]);
+        pv[x][j] = p * pv[x][j];
       }
     }
     if constexpr (MAT && !M) pf = praw;
@@ -913,12 +924,84 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       }
       f32x4 sv[KB][2], pv[KB][2];
       bf16x8 pf[KB], sf[KB];
-      sdp(cur[0], cur[1], lcur, pb, sv, pv, kFoldD);
+      sdp(cur[0], cur[1], lcur, pb, sv, pv);
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        softmax(lcur, pcur, pb, qp0, kj + 16 * kb, sv[kb], pv[kb], pf[kb], sf[kb], mask, kFoldD);
+      for (int kb = 0; kb < KB; ++kb) softmax(lcur, pcur, pb, qp0, kj + 16 * kb, sv[kb], pv[kb], pf[kb], sf[kb], mask);
       if constexpr (AQ) put_ds(dcur, pb, sf[0]);
       dvdk(cur[0], cur[1], pb, pf, sf);
+    }
+    __syncthreads();
+  };
+  // KL steps (one pair block of 32 queries, every tile): one code path for
+  // interior and masked tiles (two step forms measured about 400 bytes of
+  // spills per lane). The exponentials of both key blocks, then one
+  // wave-uniform branch around the mask selects (diagonal and last tiles),
+  // with the first transposed reads of the dV/dK products issued before it.
+  // Schedule: the S/dP products with their row reads eight ahead; the dV/dK
+  // products with four transposed reads up front, then one per product.
+  // Blocks whose queries all precede the wave's keys are computed and
+  // masked (P = 0) rather than skipped: the diagonal tiles are a few of a
+  // workgroup's.
+  auto step_kl = [&](int it, bf16 (&cur)[2][TSZ], float (&lcur)[2][BQ], bf16 (&nxt)[2][TSZ], float (&lnxt)[2][BQ])
+      __attribute__((always_inline)) {
+    const int qt0 = q_begin + it * BQ;
+    if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, ptA);
+    const bool need_mask = (CAUSAL && qt0 < k0 + BKV) || qt0 + BQ > n;
+    f32x4 sv[KB][2], pv[KB][2];
+    sdp(cur[0], cur[1], lcur, 0, sv, pv);
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      const f32x4 l4 = *(const f32x4*)&lcur[0][16 * x + 4 * g];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sv[kb][x][j] = exp2_fast(fmaf(sv[kb][x][j], sl2, -l4[j]));
+    }
+    const bf16x8 oa0 = tr_read16p<D>(cur[1], 0, 0, g, c), qa0 = tr_read16p<D>(cur[0], 0, 0, g, c);
+    ATTN_SCHED(kSchedDSRead, 8);
+#pragma unroll
+    for (int i = 0; i < 8 * TD; ++i) {
+      ATTN_SCHED(kSchedMFMA, 1);
+      ATTN_SCHED(kSchedDSRead, 1);
+    }
+    if (need_mask) {
+      // valid queries qbase + j: lo <= j <= hi
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        const int qbase = qt0 + 16 * x + 4 * g;
+        const int hi = n - 1 - qbase;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+          const int lo = CAUSAL ? kj + 16 * kb - qbase : -1;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) sv[kb][x][j] = (j < lo || j > hi) ? 0.f : sv[kb][x][j];
+        }
+      }
+    }
+    bf16x8 pf[KB], sf[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) pv[kb][x][j] = sv[kb][x][j] * pv[kb][x][j];
+      pf[kb] = frag16(sv[kb][0], sv[kb][1]);
+      sf[kb] = frag16(pv[kb][0], pv[kb][1]);
+    }
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const bf16x8 oa = db == 0 ? oa0 : tr_read16p<D>(cur[1], 0, db, g, c);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) mma16(dv[kb][db], oa, pf[kb]);
+      const bf16x8 qa = db == 0 ? qa0 : tr_read16p<D>(cur[0], 0, db, g, c);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) mma16(dk[kb][db], qa, sf[kb]);
+    }
+    ATTN_SCHED(kSchedDSRead, 4);
+#pragma unroll
+    for (int i = 0; i < 2 * KB * NDB; ++i) {
+      ATTN_SCHED(kSchedMFMA, 1);
+      ATTN_SCHED(kSchedDSRead, 1);
     }
     __syncthreads();
   };
@@ -933,15 +1016,15 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, pnxt);
     dq_prev(it, dprev);
     f32x4 sv[2][KB][2], pv[2][KB][2];
-    sdp(cur[0], cur[1], lcur, 0, sv[0], pv[0], std::false_type{});
+    sdp(cur[0], cur[1], lcur, 0, sv[0], pv[0]);
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
-      if (pb + 1 < NPB) sdp(cur[0], cur[1], lcur, pb + 1, sv[(pb + 1) & 1], pv[(pb + 1) & 1], std::false_type{});
+      if (pb + 1 < NPB) sdp(cur[0], cur[1], lcur, pb + 1, sv[(pb + 1) & 1], pv[(pb + 1) & 1]);
       bf16x8 pf[KB], sf[KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
         softmax(lcur, pcur, pb, qt0 + 32 * pb, kj + 16 * kb, sv[pb & 1][kb], pv[pb & 1][kb], pf[kb], sf[kb],
-                std::false_type{}, std::false_type{});
+                std::false_type{});
       if constexpr (AQ) put_ds(dcur, pb, sf[0]);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
@@ -983,7 +1066,9 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
                           (!(MAT || AQ) || k0 + BKV <= n);
     // the pipelined form pays off at d = 128 when S is recomputed; at smaller
     // d a pair block has too few products to hide the exponentials behind
-    if constexpr (D == 128 && !MAT && KB == 1) {
+    if constexpr (KL) {
+      step_kl(it, cur, lcur, nxt, lnxt);
+    } else if constexpr (D == 128 && !MAT && KB == 1) {
       if (interior) step_inner(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev);
       else step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::true_type{});
     } else {
