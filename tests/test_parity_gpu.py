@@ -78,12 +78,15 @@ def test_ragged_lengths(dtype, d, causal):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("scale", [-0.3, 0.0, 1.7])
-def test_scale_values(dtype, scale):
-    """Negative, zero and large scales (zero gives uniform attention)."""
-    w = workloads.Workload(f"scale_{dtype}", 1, 2, 200, 64, dtype, True, 1.0, 1.0, 1.0, 77)
+@pytest.mark.parametrize("d,causal", [(64, True), (128, True), (128, False)])
+def test_scale_values(dtype, scale, d, causal):
+    """Negative, zero and large scales (zero gives uniform attention); at
+    d = 128 the bf16 dK/dV kernel takes a negative scale as the sign of
+    s log2(e) instead of a sign flip of K."""
+    w = workloads.Workload(f"scale_{dtype}_d{d}", 1, 2, 200, d, dtype, causal, 1.0, 1.0, 1.0, 77 + d)
     inp = workloads.generate(w)
-    errs, _ = _full_compare(w, inp, True, scale=scale)
-    _check(errs, dtype, f"scale={scale} {dtype}")
+    errs, _ = _full_compare(w, inp, causal, scale=scale)
+    _check(errs, dtype, f"scale={scale} {dtype} d={d} causal={causal}")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
