@@ -8,7 +8,7 @@ namespace attn {
 
 template <int D, bool CAUSAL, bool MAT, bool AQ>
 void launch_dkdv16(BwdArgs a, int heads, hipStream_t st) {
-  constexpr int kb = dkdv16_kb(D, MAT || AQ), nw = dkdv16_nw(D, MAT, AQ), bq = dkdv16_bq(D, MAT);
+  constexpr int kb = dkdv16_kb(D, MAT, AQ), nw = dkdv16_nw(D, MAT, AQ), bq = dkdv16_bq(D, MAT);
   constexpr int bkv = 16 * kb * nw;
   a.ntiles = (a.n + bkv - 1) / bkv;
   a.nblocks = heads * a.ntiles;

@@ -687,7 +687,7 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   constexpr int KW = 16 * KB;   // keys per wave: KB blocks of 16 share every Q / dO operand read
   constexpr int BKV = KW * NW, NPB = BQ / 32, TD = D / 32, NDB = D / 16;
   static_assert(!(MAT && AQ), "the materialising backward has its own dQ pass");
-  static_assert(KB == 1 || !(MAT || AQ), "the materialising and atomic-dQ forms use 16-key waves");
+  static_assert(KB == 1 || !AQ, "the atomic-dQ form uses 16-key waves");
   constexpr int PT = MAT ? BQ * BKV : 8;
   constexpr int DST = AQ ? BKV * BQ : 8;   // dS^T tile [BKV keys][BQ queries]
   constexpr int KBL = AQ ? BKV * D : 8;    // the workgroup's K block [BKV][D]
@@ -701,7 +701,7 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 dsA[DST];
   __shared__ __attribute__((aligned(16))) bf16 dsB[DST];
   __shared__ __attribute__((aligned(16))) bf16 kbl[KBL];
-  constexpr bool KL = KB > 1 && D > 64;
+  constexpr bool KL = KB > 1 && D > 64 && !MAT;
   static_assert(!KL || BQ == 32, "the KL step takes one pair block of queries");
   __shared__ __attribute__((aligned(16))) bf16 kst[KL ? BKV * Pad16<D>::RS : 8];
 
@@ -813,14 +813,15 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       }
     }
   };
-  // P = 2^(S sl2 - L) (MAT: P from the staged block), dS = P (dP - D) as
-  // bf16 operands for the lane's key `key` (pv holds dP - D); with MASK,
-  // queries >= n, keys >= n and (causal) queries before the key get P = 0
-  auto softmax = [&](const float (&lr)[2][BQ], const bf16* pt, int pb, int qp0, int key, f32x4 (&sv)[2],
+  // P = 2^(S sl2 - L) (MAT: P from the staged block, 16-key column block
+  // kblk of the workgroup), dS = P (dP - D) as bf16 operands for the lane's
+  // key `key` (pv holds dP - D); with MASK, queries >= n, keys >= n and
+  // (causal) queries before the key get P = 0
+  auto softmax = [&](const float (&lr)[2][BQ], const bf16* pt, int pb, int qp0, int key, int kblk, f32x4 (&sv)[2],
                      f32x4 (&pv)[2], bf16x8& pf, bf16x8& sf, auto mask) __attribute__((always_inline)) {
     constexpr bool M = decltype(mask)::value;
     bf16x8 praw;
-    if constexpr (MAT) praw = tr_read16<BKV, BQ>(pt, 32 * pb, w, g, c);
+    if constexpr (MAT) praw = tr_read16<BKV, BQ>(pt, 32 * pb, kblk, g, c);
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
       f32x4 l4;
@@ -926,7 +927,8 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       bf16x8 pf[KB], sf[KB];
       sdp(cur[0], cur[1], lcur, pb, sv, pv);
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) softmax(lcur, pcur, pb, qp0, kj + 16 * kb, sv[kb], pv[kb], pf[kb], sf[kb], mask);
+      for (int kb = 0; kb < KB; ++kb)
+        softmax(lcur, pcur, pb, qp0, kj + 16 * kb, KB * w + kb, sv[kb], pv[kb], pf[kb], sf[kb], mask);
       if constexpr (AQ) put_ds(dcur, pb, sf[0]);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
@@ -1023,8 +1025,8 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       bf16x8 pf[KB], sf[KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
-        softmax(lcur, pcur, pb, qt0 + 32 * pb, kj + 16 * kb, sv[pb & 1][kb], pv[pb & 1][kb], pf[kb], sf[kb],
-                std::false_type{});
+        softmax(lcur, pcur, pb, qt0 + 32 * pb, kj + 16 * kb, KB * w + kb, sv[pb & 1][kb], pv[pb & 1][kb], pf[kb],
+                sf[kb], std::false_type{});
       if constexpr (AQ) put_ds(dcur, pb, sf[0]);
       dvdk(cur[0], cur[1], pb, pf, sf);
     }
@@ -1072,8 +1074,14 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       if (interior) step_inner(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev);
       else step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::true_type{});
     } else {
-      if (interior && (MAT || KB > 1)) step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::false_type{});
-      else step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::true_type{});
+      // the materialising form with 32-key waves at d = 128 takes the masked
+      // step on every tile: a second step form spilled about 400 bytes per
+      // lane there
+      constexpr bool one_form = MAT && KB > 1 && D > 64;
+      if (interior && (MAT || KB > 1) && !one_form)
+        step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::false_type{});
+      else
+        step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::true_type{});
     }
   };
   for (int it = 0; it < nt; it += 2) {
