@@ -658,12 +658,12 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 // as B operands, dK^T and dV^T accumulators of 16 columns per block). Every
 // Q / dO operand read from LDS feeds the KB blocks' products, so KB = 2
 // halves the LDS bytes per product. V is held in registers; K too, except at
-// d = 128 with KB = 2 (KL), where the K operands are read from an LDS copy of
-// the workgroup's key block, staged once: in registers they would take 32 of
-// the VGPRs that two waves per SIMD leave (one wave's softmax VALU work
-// overlaps the other's matrix products). KL still reads 0.625x the LDS bytes
-// per product of 16-key waves. KB = 1 serves the materialising and atomic-dQ
-// forms. Q and dO tiles of BQ queries (padded rows, Pad16; with their base-2
+// d >= 64 (KL: KB = 2 at d = 128, KB = 3 at d = 64), where the K operands are
+// read from an LDS copy of the workgroup's key block, staged once: in
+// registers they would take VGPRs that two waves per SIMD do not leave (one
+// wave's softmax VALU work overlaps the other's matrix products). At d = 128
+// KL reads 0.625x the LDS bytes per product of 16-key waves. KB = 1 serves
+// the atomic-dQ form and the materialising form at d <= 64. Q and dO tiles of BQ queries (padded rows, Pad16; with their base-2
 // LSE and -D rows) are staged in LDS;
 // every 32 queries form one k step of the dV/dK products:
 //   S = Q K^T, dP - D = dO V^T - D   (two 16-query blocks each; the dP
@@ -701,8 +701,9 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 dsA[DST];
   __shared__ __attribute__((aligned(16))) bf16 dsB[DST];
   __shared__ __attribute__((aligned(16))) bf16 kbl[KBL];
-  constexpr bool KL = KB > 1 && D > 64 && !MAT;
+  constexpr bool KL = KB > 1 && D >= 64 && !MAT;
   static_assert(!KL || BQ == 32, "the KL step takes one pair block of queries");
+  static_assert(KL || (BKV & (BKV - 1)) == 0, "the staged P block reads need a power-of-two key block");
   __shared__ __attribute__((aligned(16))) bf16 kst[KL ? BKV * Pad16<D>::RS : 8];
 
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15;
@@ -860,28 +861,30 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
   // that share it; one float32 atomic add per element
   float* dQacc = AQ ? a.dqacc + (size_t)head * n * D : nullptr;
   auto dq_products = [&](const bf16* dsT, int qt0p) __attribute__((always_inline)) {
-    constexpr int NDT = D / 16, NQT = BQ / 16;
-    constexpr int WPD = AQ ? NW / NDT : 1, QPW = NQT / WPD;
-    static_assert(!AQ || (NW % NDT == 0 && NQT % WPD == 0), "dQ tiles must split evenly over the waves");
-    const int dblk = w % NDT, qbase = (w / NDT) * QPW;
-    // lane indexes made opaque here so that nothing of this phase is hoisted
-    // out of the loop into registers that stay live across the other phases
-    int gg = g, cc = c;
-    asm volatile("" : "+v"(gg), "+v"(cc));
-    bf16x8 kfr[BKV / 32];
-#pragma unroll
-    for (int kb = 0; kb < BKV / 32; ++kb) kfr[kb] = tr_read16<D, BKV>(kbl, 32 * kb, dblk, gg, cc);
-    // rows qt0p + 16 (qbase + i) + 4 gg + j of column 16 dblk + cc
-    float* base = dQacc + (size_t)(qt0p + 16 * qbase + 4 * gg) * D + 16 * dblk + cc;
-    const int qrow = qt0p + 16 * qbase + 4 * gg;
-#pragma unroll
-    for (int i = 0; i < QPW; ++i) {
-      f32x4 acc = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < BKV / 32; ++kb) mma16(acc, tr_read16<BQ, BKV>(dsT, 32 * kb, qbase + i, gg, cc), kfr[kb]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (qrow + 16 * i + j < n) unsafeAtomicAdd(base + (16 * i + j) * D, acc[j]);
+    if constexpr (AQ) {   // (not instantiated otherwise: its reads need power-of-two tiles)
+      constexpr int NDT = D / 16, NQT = BQ / 16;
+      constexpr int WPD = AQ ? NW / NDT : 1, QPW = NQT / WPD;
+      static_assert(!AQ || (NW % NDT == 0 && NQT % WPD == 0), "dQ tiles must split evenly over the waves");
+      const int dblk = w % NDT, qbase = (w / NDT) * QPW;
+      // lane indexes made opaque here so that nothing of this phase is hoisted
+      // out of the loop into registers that stay live across the other phases
+      int gg = g, cc = c;
+      asm volatile("" : "+v"(gg), "+v"(cc));
+      bf16x8 kfr[BKV / 32];
+  #pragma unroll
+      for (int kb = 0; kb < BKV / 32; ++kb) kfr[kb] = tr_read16<D, BKV>(kbl, 32 * kb, dblk, gg, cc);
+      // rows qt0p + 16 (qbase + i) + 4 gg + j of column 16 dblk + cc
+      float* base = dQacc + (size_t)(qt0p + 16 * qbase + 4 * gg) * D + 16 * dblk + cc;
+      const int qrow = qt0p + 16 * qbase + 4 * gg;
+  #pragma unroll
+      for (int i = 0; i < QPW; ++i) {
+        f32x4 acc = (f32x4){0.f, 0.f, 0.f, 0.f};
+  #pragma unroll
+        for (int kb = 0; kb < BKV / 32; ++kb) mma16(acc, tr_read16<BQ, BKV>(dsT, 32 * kb, qbase + i, gg, cc), kfr[kb]);
+  #pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (qrow + 16 * i + j < n) unsafeAtomicAdd(base + (16 * i + j) * D, acc[j]);
+      }
     }
   };
   auto dvdk = [&](const bf16* ql, const bf16* dol, int pb, const bf16x8 (&pf)[KB], const bf16x8 (&sf)[KB])
@@ -962,7 +965,7 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     const bf16x8 oa0 = tr_read16p<D>(cur[1], 0, 0, g, c), qa0 = tr_read16p<D>(cur[0], 0, 0, g, c);
     ATTN_SCHED(kSchedDSRead, 8);
 #pragma unroll
-    for (int i = 0; i < 8 * TD; ++i) {
+    for (int i = 0; i < 4 * TD * KB; ++i) {
       ATTN_SCHED(kSchedMFMA, 1);
       ATTN_SCHED(kSchedDSRead, 1);
     }

@@ -9,21 +9,25 @@
 
 namespace attn {
 
-// dK/dV tiles. 4-wave workgroups of 32 keys per wave (two 16-key blocks:
-// every Q / dO operand read feeds two products): 64 queries per step for
-// d <= 64; 32 at d = 128, where the fused form reads K from an LDS copy of
-// the workgroup's 128 keys (36 KB) and the 32-query Q and dO stages leave
-// room for two workgroups per CU. With 4 waves, the two waves that share a
-// SIMD come from two workgroups whose barriers are independent, so one can
-// run its matrix products while the other waits or runs its softmax. The
-// materialising form (no K; the staged block of the stored P instead) takes
-// the same tiling at d = 128 and 16-key waves on 32-query tiles for
-// d <= 64 (its LDS then leaves room for two workgroups per CU). The
-// atomic-dQ form uses 8 waves of 16 keys (its dQ tiling needs 8 waves).
+// dK/dV tiles. 4-wave workgroups with several 16-key blocks per wave
+// (every Q / dO operand read feeds one product per block): 32 keys per wave
+// on 64-query steps at d = 32; 48 keys on 32-query steps at d = 64 and 32
+// keys on 32-query steps at d = 128, where the fused form reads K from an
+// LDS copy of the workgroup's 192 or 128 keys (30 or 36 KB) and the
+// 32-query Q and dO stages leave room for two workgroups per CU. With 4
+// waves, the two waves that share a SIMD come from two workgroups whose
+// barriers are independent, so one can run its matrix products while the
+// other waits or runs its softmax. The materialising form (no K; the staged
+// block of the stored P instead) takes the fused tiling at d = 128 and
+// 16-key waves on 32-query tiles for d <= 64 (its LDS then leaves room for
+// two workgroups per CU). The atomic-dQ form uses 8 waves of 16 keys (its
+// dQ tiling needs 8 waves).
 constexpr int kDkv16BQ = 64;
-constexpr int dkdv16_kb(int d, bool mat, bool aq) { return (aq || (mat && d <= 64)) ? 1 : 2; }
+constexpr int dkdv16_kb(int d, bool mat, bool aq) {
+  return (aq || (mat && d <= 64)) ? 1 : (d == 64 ? 3 : 2);
+}
 constexpr int dkdv16_nw(int d, bool mat, bool aq) { return aq ? 8 : 4; }
-constexpr int dkdv16_bq(int d, bool mat) { return (mat || d > 64) ? 32 : kDkv16BQ; }
+constexpr int dkdv16_bq(int d, bool mat) { return (mat || d >= 64) ? 32 : kDkv16BQ; }
 constexpr int dkdv16_bkv(int d, bool mat, bool aq) { return 16 * dkdv16_kb(d, mat, aq) * dkdv16_nw(d, mat, aq); }
 // queries per dQ workgroup (as in the forward)
 constexpr int kDqBQ = 128;
