@@ -663,7 +663,7 @@ __global__ void __launch_bounds__(256) dkdv_kernel(const BwdArgs a) {
 // registers they would take VGPRs that two waves per SIMD do not leave (one
 // wave's softmax VALU work overlaps the other's matrix products). At d = 128
 // KL reads 0.625x the LDS bytes per product of 16-key waves. KB = 1 serves
-// the atomic-dQ form and the materialising form at d <= 64. Q and dO tiles of BQ queries (padded rows, Pad16; with their base-2
+// the atomic-dQ form and the materialising form at d = 32. Q and dO tiles of BQ queries (padded rows, Pad16; with their base-2
 // LSE and -D rows) are staged in LDS;
 // every 32 queries form one k step of the dV/dK products:
 //   S = Q K^T, dP - D = dO V^T - D   (two 16-query blocks each; the dP
@@ -1077,10 +1077,10 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
       if (interior) step_inner(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev);
       else step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::true_type{});
     } else {
-      // the materialising form with 32-key waves at d = 128 takes the masked
+      // the materialising form with 32-key waves (d >= 64) takes the masked
       // step on every tile: a second step form spilled about 400 bytes per
-      // lane there
-      constexpr bool one_form = MAT && KB > 1 && D > 64;
+      // lane at d = 128
+      constexpr bool one_form = MAT && KB > 1 && D >= 64;
       if (interior && (MAT || KB > 1) && !one_form)
         step_seq(it, cur, lcur, pcur, dcur, nxt, lnxt, pnxt, dprev, std::false_type{});
       else

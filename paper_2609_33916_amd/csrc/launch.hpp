@@ -18,13 +18,14 @@ namespace attn {
 // waves, the two waves that share a SIMD come from two workgroups whose
 // barriers are independent, so one can run its matrix products while the
 // other waits or runs its softmax. The materialising form (no K; the staged
-// block of the stored P instead) takes the fused tiling at d = 128 and
-// 16-key waves on 32-query tiles for d <= 64 (its LDS then leaves room for
-// two workgroups per CU). The atomic-dQ form uses 8 waves of 16 keys (its
+// block of the stored P instead) runs 32-key waves on 32-query tiles at
+// d >= 64 (the fused tiling at d = 128; its P block reads need a
+// power-of-two key block, so not the 48 keys of d = 64) and 16-key waves on
+// 32-query tiles at d = 32. The atomic-dQ form uses 8 waves of 16 keys (its
 // dQ tiling needs 8 waves).
 constexpr int kDkv16BQ = 64;
 constexpr int dkdv16_kb(int d, bool mat, bool aq) {
-  return (aq || (mat && d <= 64)) ? 1 : (d == 64 ? 3 : 2);
+  return (aq || (mat && d < 64)) ? 1 : (d == 64 && !mat ? 3 : 2);
 }
 constexpr int dkdv16_nw(int d, bool mat, bool aq) { return aq ? 8 : 4; }
 constexpr int dkdv16_bq(int d, bool mat) { return (mat || d >= 64) ? 32 : kDkv16BQ; }
