@@ -16,15 +16,16 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(REPO_DIR, "include")
 LIB_NAME = "libattn_mi355x.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
-# translation units and their own flags: the bfloat16 backward kernels are
-# scheduled with the iterative ILP strategy (measured on n = 16384, d = 128
-# causal: dK/dV and dQ 2-4 % faster), the forward keeps the default strategy
-# (3 % slower under it)
+# translation units and their own flags: the bf16 dQ kernel is scheduled
+# with the iterative ILP strategy (measured on n = 16384, d = 128 causal: dQ
+# 2-4 % faster); the forward (3 % slower under it) and the bf16 dK/dV kernel
+# (2 % slower with its 32- and 48-key waves) keep the default strategy
 SOURCES = {
     "attn.hip": [],
+    "dkdv.hip": [],
     "bwd.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
 }
-DEPENDS = ["attn.hip", "bwd.hip", "launch.hpp", "kernels.hpp", "common.hpp"]
+DEPENDS = ["attn.hip", "dkdv.hip", "bwd.hip", "launch.hpp", "kernels.hpp", "common.hpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -63,8 +63,8 @@ void launch_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
   hipLaunchKernelGGL((attn::fwd_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
 }
 
-// bf16 dK/dV and dQ launch from bwd.hip (launch.hpp); float32 uses the
-// 32-key-per-wave dK/dV kernel and the dQ kernel instantiated here.
+// bf16 dK/dV and dQ launch from dkdv.hip and bwd.hip (launch.hpp); float32
+// uses the 32-key-per-wave dK/dV kernel and the dQ kernel instantiated here.
 template <typename T, int D, bool CAUSAL, bool MAT = false>
 void launch_dkdv(attn::BwdArgs a, int heads, hipStream_t st) {
   if constexpr (std::is_same<T, bf16>::value) {

@@ -1,19 +1,10 @@
-// Launches of the bfloat16 backward kernels: dK/dV (dkdv16_kernel) and dQ.
-// Compiled as a separate translation unit with its own scheduler flags; the
-// instantiations below cover every (d, causal, variant) the C ABI dispatches
-// except the atomic-dQ dK/dV kernel, which attn.hip launches itself.
+// Launches of the bfloat16 dQ kernel (fused and materialising forms).
+// Compiled as a separate translation unit with the iterative-ILP machine
+// scheduler (the build script gives each source its flags); the dK/dV
+// launches live in dkdv.hip.
 #include "launch.hpp"
 
 namespace attn {
-
-template <int D, bool CAUSAL, bool MAT, bool AQ>
-void launch_dkdv16(BwdArgs a, int heads, hipStream_t st) {
-  constexpr int kb = dkdv16_kb(D, MAT, AQ), nw = dkdv16_nw(D, MAT, AQ), bq = dkdv16_bq(D, MAT);
-  constexpr int bkv = 16 * kb * nw;
-  a.ntiles = (a.n + bkv - 1) / bkv;
-  a.nblocks = heads * a.ntiles;
-  hipLaunchKernelGGL((dkdv16_kernel<D, CAUSAL, nw, bq, MAT, AQ, kb>), dim3(a.nblocks), dim3(64 * nw), 0, st, a);
-}
 
 template <int D, bool CAUSAL, bool MAT>
 void launch_dq16(BwdArgs a, int heads, hipStream_t st) {
@@ -23,8 +14,6 @@ void launch_dq16(BwdArgs a, int heads, hipStream_t st) {
 }
 
 #define ATTN_BWD16_INST(D, C)                                                 \
-  template void launch_dkdv16<D, C, false, false>(BwdArgs, int, hipStream_t); \
-  template void launch_dkdv16<D, C, true, false>(BwdArgs, int, hipStream_t);  \
   template void launch_dq16<D, C, false>(BwdArgs, int, hipStream_t);          \
   template void launch_dq16<D, C, true>(BwdArgs, int, hipStream_t);
 

@@ -1,7 +1,8 @@
-// Launchers of the bfloat16 backward kernels (dK/dV on 16x16x32 MFMA, dQ),
-// defined in bwd.hip: a translation unit of its own, compiled with the
-// iterative-ILP machine scheduler (the build script gives each source its
-// flags), while the forward kernels keep the default scheduler.
+// Launchers of the bfloat16 backward kernels, each in a translation unit of
+// its own (the build script gives each source its flags): dK/dV on
+// 16x16x32 MFMA in dkdv.hip (default machine scheduler), dQ in bwd.hip
+// (iterative-ILP scheduler); the forward kernels, in attn.hip, keep the
+// default scheduler.
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -34,7 +35,7 @@ constexpr int dkdv16_bkv(int d, bool mat, bool aq) { return 16 * dkdv16_kb(d, ma
 constexpr int kDqBQ = 128;
 
 // MAT: the backward of the materialising path; AQ: dQ by atomics (not
-// instantiated in bwd.hip: the atomic-dQ form is launched from attn.hip)
+// instantiated in dkdv.hip: the atomic-dQ form is launched from attn.hip)
 template <int D, bool CAUSAL, bool MAT, bool AQ>
 void launch_dkdv16(BwdArgs a, int heads, hipStream_t st);
 
