@@ -952,6 +952,10 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     const int qt0 = q_begin + it * BQ;
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, ptA);
     const bool need_mask = (CAUSAL && qt0 < k0 + BKV) || qt0 + BQ > n;
+    // the S/dP products and exponentials at a raised wave priority: when both
+    // waves of a SIMD can issue, the one producing its next P and dS goes
+    // first (dK/dV 1-3 % faster)
+    __builtin_amdgcn_s_setprio(1);
     f32x4 sv[KB][2], pv[KB][2];
     sdp(cur[0], cur[1], lcur, 0, sv, pv);
 #pragma unroll
@@ -962,6 +966,7 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) sv[kb][x][j] = exp2_fast(fmaf(sv[kb][x][j], sl2, -l4[j]));
     }
+    __builtin_amdgcn_s_setprio(0);
     const bf16x8 oa0 = tr_read16p<D>(cur[1], 0, 0, g, c), qa0 = tr_read16p<D>(cur[0], 0, 0, g, c);
     ATTN_SCHED(kSchedDSRead, 8);
 #pragma unroll
@@ -1206,6 +1211,10 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) dq_kernel(const B
     for (int kb = 0; kb < NKB; ++kb) {
       const int kb0 = kv0 + 32 * kb;
       if (CAUSAL && kb0 > qw0 + 31) continue;  // every key of the block follows every query
+      // S, dP and dS at a raised wave priority, the dQ products at the normal
+      // one: when both waves of a SIMD can issue, the one producing its next
+      // dS goes first (dQ about 2 % faster at n = 16384 and at d = 64)
+      __builtin_amdgcn_s_setprio(1);
       f32x16 s = zero16(), dp = zero16();
 #pragma unroll
       for (int t = 0; t < D / (2 * KP); ++t) {
@@ -1234,6 +1243,7 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) dq_kernel(const B
         }
         dp[j] = p * (dp[j] + dq_);   // dq_ holds -D
       }
+      __builtin_amdgcn_s_setprio(0);
 #pragma unroll
       for (int t = 0; t < T32; ++t) {
         const Frag sf = FragFromAcc<T>::get(dp, t);
