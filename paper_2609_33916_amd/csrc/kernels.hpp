@@ -1020,10 +1020,10 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     }
     __syncthreads();
   };
-  // Interior tiles (every query sees every key of the workgroup, all rows
-  // valid): software-pipelined, the S/dP products of pair block pb + 1 are
-  // issued next to the exponentials of pair block pb, whose dV/dK products
-  // follow.
+  // Interior tiles of the 16-key form at d = 128 (the atomic-dQ form; every
+  // query sees every key of the workgroup, all rows valid): software-
+  // pipelined, the S/dP products of pair block pb + 1 are issued next to the
+  // exponentials of pair block pb, whose dV/dK products follow.
   auto step_inner = [&](int it, bf16 (&cur)[2][TSZ], float (&lcur)[2][BQ], bf16 (&pcur)[PT], bf16 (&dcur)[DST],
                         bf16 (&nxt)[2][TSZ], float (&lnxt)[2][BQ], bf16 (&pnxt)[PT], bf16 (&dprev)[DST])
       __attribute__((always_inline)) {
@@ -1079,8 +1079,9 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     const int qt0 = q_begin + it * BQ;
     const bool interior = qt0 + BQ <= n && (!CAUSAL || qt0 >= k0 + BKV - 1) &&
                           (!(MAT || AQ) || k0 + BKV <= n);
-    // the pipelined form pays off at d = 128 when S is recomputed; at smaller
-    // d a pair block has too few products to hide the exponentials behind
+    // KL: one step form for every tile. The 16-key form at d = 128 pipelines
+    // its interior tiles (at smaller d a pair block has too few products to
+    // hide the exponentials behind)
     if constexpr (KL) {
       step_kl(it, cur, lcur, nxt, lnxt);
     } else if constexpr (D == 128 && !MAT && KB == 1) {
