@@ -957,12 +957,15 @@ __global__ void __launch_bounds__(64 * NW, 2) dkdv16_kernel(const BwdArgs a) {
     const int qt0 = q_begin + it * BQ;
     if (it + 1 < nt) load_rows(qt0 + BQ, nxt, lnxt, ptA);
     const bool need_mask = (CAUSAL && qt0 < k0 + BKV) || qt0 + BQ > n;
-    // the S/dP products and exponentials at a raised wave priority: when both
-    // waves of a SIMD can issue, the one producing its next P and dS goes
-    // first (dK/dV 1-3 % faster)
+    // the S/dP products (at d = 64 also the exponentials) at a raised wave
+    // priority: when both waves of a SIMD can issue, the one producing its
+    // next P and dS goes first (dK/dV 1-3 % faster; at d = 128 another 2-5 %
+    // with the exponentials back at the normal priority, which at d = 64
+    // measured 8 % slower)
     __builtin_amdgcn_s_setprio(1);
     f32x4 sv[KB][2], pv[KB][2];
     sdp(cur[0], cur[1], lcur, 0, sv, pv);
+    if constexpr (D > 64) __builtin_amdgcn_s_setprio(0);
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
       const f32x4 l4 = *(const f32x4*)&lcur[0][16 * x + 4 * g];
