@@ -21,6 +21,7 @@ namespace {
 using attn::bf16;
 
 constexpr int kFwdBQ = attn::kDqBQ;  // queries per forward / dQ workgroup
+constexpr int kFwdPpBQ = 256;        // queries per ping-pong forward workgroup
 constexpr int kDkvBKV = 128;  // keys per float32 dK/dV workgroup
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
@@ -56,11 +57,21 @@ ScaleParts split_scale(float scale, int dtype) {
   return s;
 }
 
+// bf16 at d = 128: the ping-pong forward (256 queries per eight-wave
+// workgroup); otherwise the four-wave forward (128 queries per workgroup).
+// At d <= 64 a tile's softmax arithmetic outlasts its products, so the
+// ping-pong phases would wait on the softmax.
 template <typename T, int D, bool CAUSAL>
 void launch_fwd(attn::FwdArgs a, int heads, hipStream_t st) {
-  a.ntiles = (a.n + kFwdBQ - 1) / kFwdBQ;
-  a.nblocks = heads * a.ntiles;
-  hipLaunchKernelGGL((attn::fwd_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
+  if constexpr (std::is_same<T, bf16>::value && D == 128) {
+    a.ntiles = (a.n + kFwdPpBQ - 1) / kFwdPpBQ;
+    a.nblocks = heads * a.ntiles;
+    hipLaunchKernelGGL((attn::fwd_pp_kernel<D, CAUSAL>), dim3(a.nblocks), dim3(512), 0, st, a);
+  } else {
+    a.ntiles = (a.n + kFwdBQ - 1) / kFwdBQ;
+    a.nblocks = heads * a.ntiles;
+    hipLaunchKernelGGL((attn::fwd_kernel<T, D, CAUSAL>), dim3(a.nblocks), dim3(256), 0, st, a);
+  }
 }
 
 // bf16 dK/dV and dQ launch from dkdv.hip and bwd.hip (launch.hpp); float32

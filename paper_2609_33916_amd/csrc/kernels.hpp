@@ -303,6 +303,259 @@ __global__ void __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) fwd_kernel(const 
 }
 
 // ======================================================================
+// Ping-pong forward (bf16): eight-wave workgroups of 256 queries in two
+// groups of four waves. Waves w and w + 4 run on the same SIMD, one from
+// each group, and a barrier after every phase keeps the groups half a key
+// tile apart, so that on every SIMD one wave runs matrix products while the
+// other runs the softmax arithmetic:
+//   phase 2j:     group 0: G(j)       group 1: X(j - 1)
+//   phase 2j + 1: group 0: X(j)       group 1: G(j)
+// G(j) holds the score products of key tile j and the P V products of tile
+// j - 1; X(j) the mask, row maximum, rescale and exponentials of tile j.
+// Group 0 issues the copies of K(j + 1) and V(j) at the start of its G(j)
+// and waits for them at the barrier after its X(j), two phases later;
+// group 1 issues none. A tile slot is refilled only after the barrier that
+// follows the last phase reading it. Wave w of group g = w / 4 owns the 32
+// queries of block 2 (w % 4) + g, so the two waves of a SIMD see
+// neighbouring query blocks and, under a causal mask, nearly the same keys.
+// ======================================================================
+// Tile copies of the ping-pong forward: the per-lane byte offsets of a full
+// tile and of the one tile of the sequence that can end past row n - 1 (its
+// rows >= n fetch row n - 1, as in TileLoader), so a copy costs one select
+// per instruction instead of the clamp arithmetic.
+template <int D, bool P> struct PpCopy {
+  using L = TileLoader<bf16, 64, D, P>;
+  static constexpr int NI = L::NI;
+  unsigned off[NI], offr[NI];
+  int rrow;   // first row of the tile that ends past row n - 1 (-1: none)
+  __device__ __forceinline__ PpCopy(int w, int lane, int n) {
+    const L ld(w, lane);
+    rrow = (n % 64) ? n - n % 64 : -1;
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      if constexpr (P) {
+        off[j] = ld.off[j];
+        const int over = rrow + ld.xr[j] - (n - 1);
+        offr[j] = (ld.off[j] != L::kSpare && over > 0) ? ld.off[j] - 2u * (unsigned)(over * D) : ld.off[j];
+      } else {
+        off[j] = 2u * (unsigned)ld.off[j];
+        const int over = rrow + ld.xr[j] - (n - 1);
+        offr[j] = over > 0 ? 2u * (unsigned)(ld.off[j] - over * D) : off[j];
+      }
+    }
+  }
+  __device__ __forceinline__ void issue(bf16* lds, const bf16* g, int row0, int w) const {
+    const auto rs = dma_rsrc(g + (size_t)row0 * D);
+    const bool rag = row0 == rrow;
+#pragma unroll
+    for (int j = 0; j < NI; ++j) dma16(rs, rag ? offr[j] : off[j], (ATTN_LDS void*)(lds + 512 * (w * NI + j)));
+  }
+};
+
+__device__ __forceinline__ void phase_barrier() {
+  // LDS reads complete (lgkmcnt(0)), no wait for outstanding tile copies
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int D, bool CAUSAL>
+__global__ void __launch_bounds__(512) fwd_pp_kernel(const FwdArgs a) {
+  using T = bf16;
+  constexpr int BQ = 256, BKV = 64, NKB = BKV / 32, NDB = D / 32, TD = D / 16, T32 = 2;
+  static constexpr bool P32 = D == 128;
+  using TL = Tile<T, BKV, D, P32>;
+  // K and V slots in distinct LDS objects (loop unrolled by two), so that
+  // reads of one slot never wait for a copy into the other
+  __shared__ __attribute__((aligned(16))) T kA[TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) T kB[TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) T vA[TL::ELEMS];
+  __shared__ __attribute__((aligned(16))) T vB[TL::ELEMS];
+
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, c = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = w >> 2, wi = w & 3;
+  int head, qt;
+  block_map(blockIdx.x, a.nblocks, a.ntiles, CAUSAL, head, qt);
+  const int n = a.n;
+  const size_t hoff = (size_t)head * (size_t)a.head_stride;
+  const T* Qg = (const T*)a.q + hoff;
+  const T* Kg = (const T*)a.k + hoff;
+  const T* Vg = (const T*)a.v + hoff;
+  const int q0 = qt * BQ, qw0 = q0 + 32 * (2 * wi + g), qi = qw0 + c;
+
+  RowFrags<T, D> qf;
+  qf.load(Qg, qi, n, h, a.qflip);
+
+  const int kv_end = CAUSAL ? min(n, q0 + BQ) : n;
+  const int nt = (kv_end + BKV - 1) / BKV;
+
+  const PpCopy<D, P32> ld(wi, lane, n);
+  if (g == 0) ld.issue(kA, Kg, 0, wi);
+  __syncthreads();
+
+  f32x16 oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = zero16();
+  f32x16 s[NKB];
+  bf16x8 pf[NKB][T32];
+  float m_use = -INFINITY, lsum = 0.f;
+  const float sl2 = a.sl2;
+
+  // G(j): scores of tile j (K in kc), then P V of tile j - 1 (V in vp).
+  // Both run on every tile from j = 1 on: the phases are as long as their
+  // slowest wave, so skipping a wave's products past its last key (causal)
+  // or past the last tile saves no time, and there X(j) masks every key, so
+  // P is zero and the extra P V adds zeros (every V slot holds finite rows
+  // from j = 1 on).
+  auto scores = [&](const T (&kc)[TL::ELEMS]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int b = 0; b < NKB; ++b) s[b] = zero16();
+#pragma unroll
+    for (int t = 0; t < TD; ++t)
+#pragma unroll
+      for (int b = 0; b < NKB; ++b) mma(s[b], RowRead<T, D, P32>::get(kc, b, t, h, c), qf.f[t]);
+  };
+  auto G = [&](const T (&kc)[TL::ELEMS], const T (&vp)[TL::ELEMS]) __attribute__((always_inline)) {
+    scores(kc);
+#pragma unroll
+    for (int b = 0; b < NKB; ++b)
+#pragma unroll
+      for (int t = 0; t < T32; ++t)
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+          mma(oacc[db], TransRead<T, D, 64, P32>::get(vp, b, db, t, h, c), pf[b][t]);
+    // operand reads kept kAhead products ahead: the wave of the other group
+    // on this SIMD is in its softmax phase and does not cover LDS latency
+    constexpr int NS = NKB * TD, NP = NKB * T32 * NDB, kAhead = 6;
+    ATTN_SCHED(kSchedDSRead, kAhead);
+#pragma unroll
+    for (int i = 0; i < NS + NP; ++i) {
+      ATTN_SCHED(kSchedMFMA, 1);
+      const int nx = i + kAhead;   // product whose operands are read next
+      if (nx < NS) ATTN_SCHED(kSchedDSRead, 1);
+      else if (nx < NS + NP) ATTN_SCHED(kSchedDSRead, 2);
+    }
+  };
+  // X(j): softmax of tile j's scores into pf. Keys at or beyond n, and under
+  // the causal mask keys after the query, are set to -inf by selection (the
+  // scores of a slot never filled may be any bit pattern), so a tile with no
+  // visible key gives P = 0 and leaves the row state unchanged.
+  auto X = [&](int j) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_setprio(1);
+    const int kv0 = j * BKV;
+    // lane (h, c): s[b][k] = raw score of key kv0 + 32b + 16h + k, query qi
+    const bool edge = (kv0 + BKV > n) || (CAUSAL && kv0 + BKV - 1 > qw0);
+    if (edge) {
+      const int last = CAUSAL ? min(qi, n - 1) : n - 1;
+#pragma unroll
+      for (int b = 0; b < NKB; ++b) {
+        const int lim = last - (kv0 + 32 * b + 16 * h);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) s[b][k] = (k > lim) ? -INFINITY : s[b][k];
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < NKB; ++b)
+#pragma unroll
+      for (int k = 0; k < 16; ++k) mx = fmaxf(mx, s[b][k]);
+    mx = halves_max(mx);
+    const float mt = mx * sl2;
+    const bool resc = mt > m_use + kRescaleThresh;
+    if (__builtin_amdgcn_ballot_w64(resc)) {
+      const float alpha = resc ? exp2_fast(m_use - mt) : 1.f;
+      if (resc) m_use = mt;
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int k = 0; k < 16; ++k) oacc[db][k] *= alpha;
+    }
+    const float mb = (m_use == -INFINITY) ? 0.f : -m_use;
+    float rs = 0.f;
+#pragma unroll
+    for (int b = 0; b < NKB; ++b) {
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const float p = exp2_fast(fmaf(s[b][k], sl2, mb));
+        rs += p;
+        s[b][k] = p;
+      }
+#pragma unroll
+      for (int t = 0; t < T32; ++t) pf[b][t] = FragFromAcc<T>::get(s[b], t);
+    }
+    lsum += rs;
+    __builtin_amdgcn_s_setprio(0);
+  };
+  // group 0 copies K(j + 1) into kn and V(j) into vc at the start of G(j)
+  auto copies = [&](int j, T (&kn)[TL::ELEMS], T (&vc)[TL::ELEMS]) __attribute__((always_inline)) {
+    if (g == 0) {
+      if (j + 1 < nt) ld.issue(kn, Kg, (j + 1) * BKV, wi);
+      if (j < nt) ld.issue(vc, Vg, j * BKV, wi);
+    }
+  };
+  // key tile j >= 1: K(j) in kc, V(j - 1) in vp
+  auto iter = [&](int j, T (&kc)[TL::ELEMS], T (&kn)[TL::ELEMS], T (&vp)[TL::ELEMS], T (&vc)[TL::ELEMS])
+      __attribute__((always_inline)) {
+    copies(j, kn, vc);
+    G(kc, vp);
+    phase_barrier();
+    X(j);
+    __syncthreads();
+  };
+  if (g == 1) phase_barrier();
+  // tile 0: scores only
+  copies(0, kB, vA);
+  scores(kA);
+  phase_barrier();
+  X(0);
+  __syncthreads();
+  for (int j = 1; j <= nt; j += 2) {
+    iter(j, kB, kA, vA, vB);
+    if (j + 1 <= nt) iter(j + 1, kA, kB, vB, vA);
+  }
+  if (g == 0) phase_barrier();
+
+  // ---- epilogue: lane (h, c) holds O^T columns of query qi
+  const float ltot = halves_sum(lsum);
+  const float inv = 1.f / ltot;
+  T* Og = (T*)a.o + hoff;
+  const T* dOg = a.dout ? (const T*)a.dout + hoff : nullptr;
+  float dpart = 0.f;
+  if (qi < n) {
+    f32x4 gd[NDB][4];
+    if (dOg) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) gd[db][q4] = Quad<T>::load(dOg + (size_t)qi * D + 32 * db + 8 * q4 + 4 * h);
+    }
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int col = 32 * db + 8 * q4 + 4 * h;
+        const float o0 = oacc[db][4 * q4 + 0] * inv, o1 = oacc[db][4 * q4 + 1] * inv;
+        const float o2 = oacc[db][4 * q4 + 2] * inv, o3 = oacc[db][4 * q4 + 3] * inv;
+        Quad<T>::store(Og + (size_t)qi * D + col, o0, o1, o2, o3);
+        if (dOg) dpart += o0 * gd[db][q4][0] + o1 * gd[db][q4][1] + o2 * gd[db][q4][2] + o3 * gd[db][q4][3];
+      }
+  }
+  const float dsum = halves_sum(dpart);
+  if (qi < n && h == 0) {
+    const size_t row = (size_t)head * n + qi;
+    const float l2 = m_use + log2f(ltot);
+    a.lse[row] = l2 * kLn2;
+    if (dOg) {
+      a.dvec[row] = -dsum;
+      a.lse2[row] = l2;
+    }
+  }
+}
+
+// ======================================================================
 // Materialising forward: the naive realisation in which the attention matrix
 // is written to memory for the backward to read (Fig. fig:concept; the A
 // array of Table tab:paper1-dram). Same tiling as fwd_kernel, two sweeps over
