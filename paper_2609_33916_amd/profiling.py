@@ -72,7 +72,8 @@ def short_name(kernel: str) -> str:
     end in MAT."""
     k = kernel.replace("void ", "")
     for key in ("decode_append_kernel", "decode_combine_kernel", "decode_kernel",
-                "mat_fwd_kernel", "bwd_prep_kernel", "zero_f32_kernel", "dq_finalize_kernel", "fwd_kernel",
+                "mat_fwd_kernel", "bwd_prep_kernel", "zero_f32_kernel", "dq_finalize_kernel", "fwd_pp_kernel",
+                "fwd_kernel",
                 "dkdv16_kernel", "dkdv_kernel", "dq_kernel", "copyBuffer", "elementwise"):
         if key in k:
             if key == "dkdv16_kernel":

@@ -17,6 +17,7 @@ def test_short_names_of_backward_kernels():
 def test_short_names_of_other_kernels():
     f = profiling.short_name
     assert f("void attn::fwd_kernel<__bf16, 128, true>(attn::FwdArgs)") == "fwd_kernel"
+    assert f("void attn::fwd_pp_kernel<128, true>(attn::FwdArgs)") == "fwd_pp_kernel"
     assert f("void attn::mat_fwd_kernel<__bf16, 128, true>(attn::FwdArgs)") == "mat_fwd_kernel"
     assert f("void attn::decode_kernel<128>(attn::DecArgs)") == "decode_kernel"
     assert f("void attn::decode_combine_kernel<__bf16, 128>(float const*, void*, float*, int, int)") == \
