@@ -1797,48 +1797,58 @@ __global__ void __launch_bounds__(256) decode_kernel(const DecArgs a) {
 template <typename T, int D>
 __global__ void __launch_bounds__(256) decode_combine_kernel(const float* part, void* o, float* lse, int rows,
                                                              int nsplit) {
-  constexpr int DL = D / 4, SL = 256 / DL;           // d lanes, split lanes
-  __shared__ float red[256];
-  __shared__ __attribute__((aligned(16))) f32x4 osum[SL][DL];
-  const int row = blockIdx.x, t = threadIdx.x;
-  const float* po = part + (size_t)row * nsplit * D;
-  const float* pml = part + (size_t)rows * nsplit * D + (size_t)row * nsplit * 2;
-  // M = max_s m_s
-  float m = -INFINITY;
-  for (int s = t; s < nsplit; s += 256) m = fmaxf(m, pml[2 * s]);
-  red[t] = m;
-  __syncthreads();
-  for (int k = 128; k > 0; k >>= 1) {
-    if (t < k) red[t] = fmaxf(red[t], red[t + k]);
-    __syncthreads();
-  }
-  const float M = red[0];
-  __syncthreads();
-  const int dl = t % DL, sl = t / DL;
+  // one workgroup per query row; thread t takes 4 of the d values (dl) of
+  // the splits sl, sl + SL, ...; it folds them into its own running
+  // (max, sum, O) with the log-sum-exp rule, U splits per pass with all
+  // their loads issued before the first fold, and the SL partial states of
+  // each dl are folded together through LDS at the end
+  constexpr int DL = D / 4, SL = 256 / DL, U = 8;
+  __shared__ float smax[SL][DL], ssum[SL][DL];
+  __shared__ __attribute__((aligned(16))) f32x4 sacc[SL][DL];
+  const int row = blockIdx.x, t = threadIdx.x, dl = t % DL, sl = t / DL;
+  const float* po = part + (size_t)row * nsplit * D + 4 * dl;
+  const f32x2* pml = (const f32x2*)(part + (size_t)rows * nsplit * D + (size_t)row * nsplit * 2);
+  float mt = -INFINITY, lt = 0.f;
   f32x4 acc = (f32x4){0.f, 0.f, 0.f, 0.f};
-  float l = 0.f;
-  for (int s = sl; s < nsplit; s += SL) {
-    const float f = (M == -INFINITY) ? 0.f : exp2_fast(pml[2 * s] - M);
-    l += f * pml[2 * s + 1];
-    const f32x4 v = *(const f32x4*)(po + (size_t)s * D + 4 * dl);
-    acc += f * v;
-  }
-  osum[sl][dl] = acc;
-  red[t] = (dl == 0) ? l : 0.f;
-  __syncthreads();
-  for (int k = 128; k > 0; k >>= 1) {
-    if (t < k) red[t] += red[t + k];
-    __syncthreads();
-  }
-  const float ltot = red[0];
-  if (t < DL) {
-    f32x4 r = osum[0][t];
+  // fold one partial state (m: base-2 max, l: sum, v: unnormalised O) into (mt, lt, acc)
+  auto fold = [&](float m, float l, f32x4 v) __attribute__((always_inline)) {
+    if (m == -INFINITY) return;   // an empty split
+    const float nm = fmaxf(mt, m);
+    const float a = (mt == -INFINITY) ? 0.f : exp2_fast(mt - nm), b = exp2_fast(m - nm);
+    lt = lt * a + l * b;
+    acc = acc * a + v * b;
+    mt = nm;
+  };
+  for (int s0 = sl; s0 < nsplit; s0 += SL * U) {
+    f32x2 ml[U];
+    f32x4 v[U];
 #pragma unroll
-    for (int k = 1; k < SL; ++k) r += osum[k][t];
-    const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
-    Quad<T>::store((T*)o + (size_t)row * D + 4 * t, r[0] * inv, r[1] * inv, r[2] * inv, r[3] * inv);
+    for (int u = 0; u < U; ++u) {
+      const int s = s0 + SL * u;
+      ml[u] = (f32x2){-INFINITY, 0.f};
+      v[u] = (f32x4){0.f, 0.f, 0.f, 0.f};
+      if (s < nsplit) {
+        ml[u] = pml[s];
+        v[u] = *(const f32x4*)(po + (size_t)s * D);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) fold(ml[u][0], ml[u][1], v[u]);
   }
-  if (lse && t == 0) lse[row] = ltot > 0.f ? (M + log2f(ltot)) * kLn2 : -INFINITY;
+  smax[sl][dl] = mt;
+  ssum[sl][dl] = lt;
+  sacc[sl][dl] = acc;
+  __syncthreads();
+  if (t < DL) {
+    mt = -INFINITY;
+    lt = 0.f;
+    acc = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < SL; ++k) fold(smax[k][t], ssum[k][t], sacc[k][t]);
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    Quad<T>::store((T*)o + (size_t)row * D + 4 * t, acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+    if (lse && t == 0) lse[row] = lt > 0.f ? (mt + log2f(lt)) * kLn2 : -INFINITY;
+  }
 }
 
 // ======================================================================
