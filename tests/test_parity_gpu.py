@@ -91,10 +91,14 @@ def test_scale_values(dtype, scale, d, causal):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("causal", [False, True])
-def test_forward_entry_point(dtype, causal):
+@pytest.mark.parametrize("d", [64, 128])
+def test_forward_entry_point(dtype, causal, d):
+    """attn_fwd alone (no dO: the forward writes no D); at d = 128 in bf16
+    this is the eight-wave forward, with 333 queries ending inside its
+    second 256-query workgroup."""
     import torch
     import paper_2609_33916_amd as lib
-    w = workloads.Workload(f"fwd_{dtype}", 2, 3, 333, 64, dtype, causal, 1.0, 1.0, 1.0, 55)
+    w = workloads.Workload(f"fwd_{dtype}_d{d}", 2, 3, 333, d, dtype, causal, 1.0, 1.0, 1.0, 55 + d)
     inp = workloads.generate(w)
     dev = to_gpu(inp)
     O, L = lib.attn_fwd(dev["q"], dev["k"], dev["v"], scale=w.scale, causal=causal)
